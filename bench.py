@@ -1,0 +1,342 @@
+#!/usr/bin/env python3
+"""Benchmark of the BFP8 deferred-dequantization decode path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input, on one HIP
+stream, inputs resident in HBM:
+  * hma_decode_attn_bfp8 for every layer of the model (one decode token's
+    attention over the paged BFP8 KV of the whole batch), then
+  * hma_bfp8_dequant_pages rebuilding one request's K and V of every layer
+    into the paged BF16 cache (a single launch over all 2 x layers pools).
+For the trace mix (workload 4) every layer launch reads a page table in
+which half the pages are already BF16, and each attention launch is
+followed by the rebuild of that layer's freshly arrived BFP8 pages.
+
+Prints ONE JSON line.  value = effective KV GB/s of the step: the bytes the
+method must move (BFP8 pages at 1.0625 B/element, BF16 pages at 2 B/element,
+plus Q, output and page table; for the rebuild, BFP8 read + BF16 written)
+divided by the step time.  Per-kernel figures come from HIP events recorded
+on the launch stream around every launch.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload 3]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as wl  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+KERNEL_SOURCES = ["paper_2606_29986_amd/csrc/decode_attn.hip",
+                  "paper_2606_29986_amd/csrc/bfp8_dequant.hip",
+                  "paper_2606_29986_amd/csrc/hma_device.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_hash(path: str) -> str:
+    h = hashlib.sha256()
+    for p in (path, "paper_2606_29986_amd/csrc/hma_device.h"):
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
+
+
+# ------------------------------------------------------------ byte accounting
+
+def bfp8_bytes_per_token_layer(hkv: int, d: int = 128) -> int:
+    """K + V bytes of one token of one layer in BFP8 (1 + 1/16 B per element)."""
+    return 2 * hkv * (d + d // 16)
+
+
+def bf16_bytes_per_token_layer(hkv: int, d: int = 128) -> int:
+    return 2 * hkv * d * 2
+
+
+def attn_bytes(w: wl.Workload, ctx: np.ndarray, bf16_tokens: int = 0) -> int:
+    """Algorithmic bytes of one attention launch: KV pages read (by format),
+    Q read, output written, page-table entries and context lengths read."""
+    tokens = int(ctx.sum())
+    kv = (tokens - bf16_tokens) * bfp8_bytes_per_token_layer(w.num_kv_heads, w.head_dim) \
+        + bf16_tokens * bf16_bytes_per_token_layer(w.num_kv_heads, w.head_dim)
+    qo = 2 * w.batch * w.num_q_heads * w.head_dim * 2
+    pt = int(wl.pages_per_seq(ctx, w.page_size).sum()) * 4 + w.batch * 4
+    return kv + qo + pt
+
+
+def dequant_bytes(w: wl.Workload, n_pages: int, n_pools: int) -> int:
+    """BFP8 read + BF16 written + page ids, for n_pages pages of n_pools pools."""
+    tile = w.page_size * w.head_dim
+    per_page = w.num_kv_heads * (tile + tile // 16 + 2 * tile)
+    return n_pools * n_pages * per_page + 2 * 4 * n_pages
+
+
+# -------------------------------------------------------------- CPU baseline
+
+def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
+    """Time the float64 oracle (as it stands) on a bounded sample of the same
+    workload: whole sequences of one layer, as many as fit ~budget_s."""
+    import oracle
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from oracle_fixtures import make_paged  # test infrastructure (value draws + encode)
+    ctx_full = wl.context_lens(w)
+    n_seq = 1
+    sample_ctx = ctx_full.copy()
+    # one layer of the workload, restricted to its first sequences
+    kv = make_paged(w, value_seqs=list(range(min(4, w.batch))), with_bf16_pool=False)
+    spent, elapsed, done_tokens = 0, 0.0, 0
+    while elapsed < budget_s and n_seq <= min(4, w.batch):
+        sel = np.arange(n_seq)
+        t0 = time.perf_counter()
+        oracle.decode_attn(np.ascontiguousarray(kv.q[sel]), kv.k_mant, kv.k_exp, kv.v_mant,
+                           kv.v_exp, None, None, np.ascontiguousarray(kv.page_table[sel]),
+                           np.ascontiguousarray(kv.ctx[sel]), kv.num_kv_heads, kv.page_size,
+                           kv.scale)
+        elapsed = time.perf_counter() - t0
+        done_tokens = int(sample_ctx[sel].sum())
+        if elapsed * 2 > budget_s:
+            break
+        n_seq *= 2
+    nbytes = done_tokens * bfp8_bytes_per_token_layer(w.num_kv_heads, w.head_dim)
+    cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    return {"value": round(nbytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"float64 oracle attention, 1 layer, {n_seq} of {w.batch} sequences "
+                      f"({done_tokens} tokens, all {w.num_q_heads} heads): {elapsed:.2f} s"}
+
+
+# --------------------------------------------------------------------- main
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3)
+    ap.add_argument("--tokens-per-split", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--resident-layers", type=int, default=0,
+                    help="layers kept resident (0 = all that the workload defines, 8 for the trace mix)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+    import paper_2606_29986_amd as hma
+
+    w = wl.WORKLOADS[args.workload]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ctx = wl.context_lens(w)
+    pt_np, total_pages = wl.page_table(w, ctx)
+    max_ctx = int(ctx.max())
+    mixed = w.bf16_page_fraction > 0
+    resident = args.resident_layers or (8 if mixed else w.layers)
+    n_pools = 2 * resident
+
+    # ---- resident inputs: one allocation per stream, pool p = 2*layer + (0: K, 1: V)
+    mant = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim),
+                       dtype=torch.uint8, device=dev)
+    expo = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim // 16),
+                       dtype=torch.uint8, device=dev)
+    for layer in range(resident):
+        for kind, off in (("k", 0), ("v", 1)):
+            m, e = wl.bfp8_codes_device(w, layer, kind, total_pages, dev)
+            mant[2 * layer + off].copy_(m)
+            expo[2 * layer + off].copy_(e)
+            del m, e
+    g = torch.Generator(device=dev)
+    g.manual_seed(1000 + w.index)
+    q = torch.randn((resident, w.batch, w.num_q_heads, w.head_dim), generator=g, device=dev)
+    q = q.to(torch.bfloat16).view(torch.int16).contiguous()
+    out = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.int16, device=dev)
+    ctx_d = torch.from_numpy(ctx).to(dev)
+
+    bf16_tokens = 0
+    if mixed:
+        # BF16 pool per resident layer and stream; tagged pages read it
+        mask = wl.bf16_page_mask(w, total_pages)
+        bf16 = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim),
+                           dtype=torch.int16, device=dev)
+        bf16.random_(-32768, 32767, generator=g)
+        bf16 &= 0x3FFF                       # finite BF16 patterns
+        tagged = pt_np.copy()
+        npg = wl.pages_per_seq(ctx, w.page_size)
+        for b in range(w.batch):
+            sel = mask[pt_np[b, :npg[b]]]
+            tagged[b, :npg[b]][sel] |= wl.TAG_BF16
+            last_full = ctx[b] - (npg[b] - 1) * w.page_size
+            tok = np.full(npg[b], w.page_size)
+            tok[-1] = last_full
+            bf16_tokens += int(tok[sel].sum())
+        pt_d = torch.from_numpy(tagged).to(dev)
+        fresh = np.nonzero(~mask)[0].astype(np.int32)
+        fresh_d = torch.from_numpy(fresh).to(dev)
+        dq_pages = len(fresh)
+    else:
+        pt_d = torch.from_numpy(pt_np).to(dev)
+        # standalone rebuild of request 0 of every layer into a BF16 cache
+        req_pages = pt_np[0, :int(wl.pages_per_seq(ctx[:1], w.page_size)[0])].astype(np.int32)
+        src_d = torch.from_numpy(req_pages).to(dev)
+        dst_d = torch.arange(len(req_pages), dtype=torch.int32, device=dev)
+        dq_pages = len(req_pages)
+        bf16_dst = torch.empty((n_pools, dq_pages, w.num_kv_heads, w.page_size, w.head_dim),
+                               dtype=torch.int16, device=dev)
+    tps = args.tokens_per_split or hma.tokens_per_split(w.batch, w.num_q_heads, w.num_kv_heads,
+                                                        max_ctx)
+    ws = hma.alloc_workspace(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx, tps, device=dev)
+    scale = wl.softmax_scale(w)
+    stream = torch.cuda.current_stream()
+
+    def attn_launch(layer_slot):
+        hma.decode_attn_bfp8(
+            q[layer_slot], mant[2 * layer_slot], expo[2 * layer_slot], mant[2 * layer_slot + 1],
+            expo[2 * layer_slot + 1], pt_d, ctx_d, max_ctx, out,
+            k_bf16=bf16[2 * layer_slot] if mixed else None,
+            v_bf16=bf16[2 * layer_slot + 1] if mixed else None,
+            scale=scale, num_kv_heads=w.num_kv_heads, tokens_per_split=tps, workspace=ws,
+            stream=stream)
+
+    def dequant_launch(layer_slot=None):
+        if mixed:       # this layer's fresh pages, K and V (two pools at stride total_pages)
+            hma.bfp8_dequant_pages(mant[2 * layer_slot], expo[2 * layer_slot], bf16[2 * layer_slot],
+                                   fresh_d, fresh_d, n_pools=2, src_pool_stride_pages=total_pages,
+                                   dst_pool_stride_pages=total_pages, num_kv_heads=w.num_kv_heads,
+                                   stream=stream)
+        else:           # request 0 of every layer, K and V: one launch over all pools
+            hma.bfp8_dequant_pages(mant, expo, bf16_dst, src_d, dst_d, n_pools=n_pools,
+                                   src_pool_stride_pages=total_pages,
+                                   dst_pool_stride_pages=dq_pages, num_kv_heads=w.num_kv_heads,
+                                   stream=stream)
+
+    n_launch = w.layers
+    events = []
+
+    def step(record):
+        evs = []
+        for layer in range(n_launch):
+            slot = layer % resident
+            if record:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            attn_launch(slot)
+            if record:
+                e1 = torch.cuda.Event(enable_timing=True)
+                e1.record(stream)
+            if mixed:
+                dequant_launch(slot)
+                if record:
+                    e2 = torch.cuda.Event(enable_timing=True)
+                    e2.record(stream)
+                    evs.append((e0, e1, e2))
+            elif record:
+                evs.append((e0, e1, None))
+        if not mixed:
+            if record:
+                d0 = torch.cuda.Event(enable_timing=True)
+                d0.record(stream)
+            dequant_launch()
+            if record:
+                d1 = torch.cuda.Event(enable_timing=True)
+                d1.record(stream)
+                evs.append((d0, None, d1))
+        if record:
+            events.append(evs)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    attn_us, dq_us = [], []
+    for evs in events:
+        for e0, e1, e2 in evs:
+            if e1 is not None:
+                attn_us.append(e0.elapsed_time(e1) * 1e3)
+                if e2 is not None:
+                    dq_us.append(e1.elapsed_time(e2) * 1e3)
+            else:
+                dq_us.append(e0.elapsed_time(e2) * 1e3)
+    attn_us = np.array(attn_us)
+    dq_us = np.array(dq_us)
+
+    a_bytes = attn_bytes(w, ctx, bf16_tokens)
+    if mixed:
+        d_bytes = dequant_bytes(w, dq_pages, 2)
+        step_bytes = n_launch * (a_bytes + d_bytes)
+    else:
+        d_bytes = dequant_bytes(w, dq_pages, n_pools)
+        step_bytes = n_launch * a_bytes + d_bytes
+    ms_per_step = wall / args.steps * 1e3
+    value = step_bytes / (wall / args.steps) / 1e9
+    attn_mean = float(attn_us.mean())
+    attn_gbps = a_bytes / (attn_mean * 1e-6) / 1e9
+
+    traffic = None
+    try:
+        tf = json.load(open(TRAFFIC_FILE))
+        ent = tf.get("decode_attn_bfp8", {}).get(w.name)
+        if ent and ent.get("kernel_hash") == kernel_hash(KERNEL_SOURCES[0]):
+            traffic = ent["bytes_per_launch"]
+    except (OSError, ValueError):
+        pass
+
+    res = {
+        "metric": "effective KV GB/s (fraction of HBM peak) + decode-attention us/layer, "
+                  "Qwen3-32B 8K",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded BFP8 codes drawn on the device; no dataset)",
+        "config": {
+            "workload": w.name, "batch": w.batch, "context": "uniform %d" % max_ctx
+            if w.ctx[0] == "uniform" else "ragged, max %d, total %d" % (max_ctx, int(ctx.sum())),
+            "layers": w.layers, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
+            "head_dim": w.head_dim, "page_size": w.page_size, "tokens_per_split": tps,
+            "resident_layers": resident, "bf16_page_fraction": w.bf16_page_fraction,
+            "step": ("attention over %d layers (mixed BF16/BFP8 pages) + per-layer rebuild of "
+                     "fresh pages" % n_launch) if mixed else
+                    ("attention over %d layers + one launch rebuilding request 0's K/V of all "
+                     "%d layers (%d pages each)" % (n_launch, w.layers, dq_pages)),
+        },
+        "attn_us_per_layer": round(attn_mean, 3),
+        "attn_us_p50": round(float(np.percentile(attn_us, 50)), 3),
+        "attn_us_p99": round(float(np.percentile(attn_us, 99)), 3),
+        "attn_GBps": round(attn_gbps, 2),
+        "attn_frac_hbm_peak": round(attn_gbps / HBM_PEAK_GBPS, 4),
+        "dequant_us": round(float(dq_us.mean()), 3),
+        "dequant_us_p99": round(float(np.percentile(dq_us, 99)), 3),
+        "dequant_GBps": round(d_bytes / (float(dq_us.mean()) * 1e-6) / 1e9, 2),
+        "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 2), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic,
+                     "kernel": "decode_attn_bfp8_kernel",
+                     "algorithmic_bytes_per_launch": a_bytes},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

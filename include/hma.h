@@ -1,0 +1,180 @@
+/*
+ * hma.h -- C ABI of libhma, the MI355X (gfx950) decode-side hot path of
+ * HMA-Serve's deferred dequantization ("HBM Is Not All You Need", arXiv
+ * 2606.29986, Sec. 3.3 and Fig. 2).
+ *
+ * KV-cache pages arrive from the prefill side as raw block-float BFP8 bytes
+ * and stay that way in HBM.  Two calls consume them:
+ *   hma_bfp8_dequant_pages  lazily rebuilds BFP8 pages into the paged BF16
+ *                           cache (Sec. 3.3: whole-request reconstruction);
+ *   hma_decode_attn_bfp8    single-token GQA decode attention that decodes
+ *                           BFP8 pages in registers inside the paged read
+ *                           (Sec. 3.3, Fig. 2), with the context split across
+ *                           workgroups and merged by log-sum-exp.
+ *
+ * BFP8 element format (the paper gives a per-block shared exponent and a
+ * 7-bit mantissa; the rest are this library's readings):
+ *   block    = 16 consecutive head-dim channels of one token of one KV head
+ *   exponent = one byte E per block (bias 127)
+ *   element  = one byte: bit 7 sign s, bits 6..0 magnitude m
+ *   value    = (-1)^s * m * 2^(E-133)   (exactly representable in BF16;
+ *              E = 255 with m >= 64 is +-Inf; m = 0 is a zero with sign s)
+ *
+ * Page layouts (head_dim D = 128, page_size P = 16, per pool):
+ *   mantissa pool  uint8  [pages][Hkv][P][D]      2048 B per (page, head)
+ *   exponent pool  uint8  [pages][Hkv][P][D/16]    128 B per (page, head)
+ *   BF16 pool      uint16 [pages][Hkv][P][D]      4096 B per (page, head)
+ * A page table entry is a page id; with HMA_PAGE_BF16 set the page lives in
+ * the BF16 pool, else in the BFP8 pools.  Logical token t of a sequence is
+ * slot t % P of the page named by entry t / P.
+ *
+ * Conventions for every call:
+ *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
+ *     every buffer.  The library keeps no pointer and no global state: calls
+ *     are reentrant and may run on different streams concurrently, provided
+ *     they do not share a workspace.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream).
+ *     No call synchronises or allocates.
+ *   - Arguments are validated on the host before any HIP call; a rejected
+ *     call enqueues nothing.  Device-resident contents (page ids in range,
+ *     context_lens[b] <= max_context_len) are the caller's contract; breaking
+ *     it is undefined behaviour.
+ *   - Return value: HMA_OK, or a negative hma_status.  HMA_EHIP means the
+ *     launch itself failed.
+ */
+#ifndef HMA_H
+#define HMA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define HMA_API __attribute__((visibility("default")))
+#else
+#define HMA_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum hma_status {
+    HMA_OK = 0,
+    HMA_EINVAL = -1,        /* NULL pointer, bad size, misalignment, aliasing */
+    HMA_EUNSUPPORTED = -2,  /* valid but not implemented: head_dim != 128, page_size != 16, g > 16 */
+    HMA_EWORKSPACE = -3,    /* workspace missing or smaller than required */
+    HMA_EHIP = -4           /* kernel launch failed */
+};
+
+#define HMA_PAGE_BF16 0x40000000     /* page-table tag: page lives in the BF16 pool */
+#define HMA_PAGE_ID_MASK 0x3FFFFFFF  /* page id bits of a page-table entry */
+
+/*
+ * hma_bfp8_dequant_pages -- lazy BFP8 -> BF16 page reconstruction
+ * (Sec. 3.3: raw BFP8 pages kept in HBM and rebuilt to BF16 on the decode
+ * GPU; the paper reports a fused whole-request rebuild).
+ *
+ * For every pool p in [0, n_pools) and pair i in [0, n_pages), the whole
+ * page src_pages[i] (all KV heads) of BFP8 pool p is decoded into page
+ * dst_pages[i] of BF16 pool p.  Pool p of the mantissa / exponent / BF16
+ * streams starts p * src_pool_stride_pages (BFP8) or
+ * p * dst_pool_stride_pages (BF16) pages after pool 0, so one call can
+ * rebuild a request's K and V of every layer when those pools sit at a fixed
+ * page stride in one allocation.  The output is bit-exact: every BF16 value
+ * is the exact value of its BFP8 element.  Pages not named in dst_pages are
+ * not touched.
+ *
+ *   src_mant   uint8 mantissa pool 0, 16-byte aligned
+ *   src_exp    uint8 exponent pool 0, 16-byte aligned
+ *   dst_bf16   uint16 BF16 pool 0, 16-byte aligned; must not overlap the
+ *              source ranges touched by this call
+ *   src_pages, dst_pages  int32 [n_pages] device arrays of page ids (ids in
+ *              range of their pools; no two pairs may name the same
+ *              destination page)
+ *   n_pages    number of page pairs (0 is a no-op)
+ *   n_pools    number of pools (>= 1 unless n_pages == 0)
+ *   num_kv_heads >= 1, head_dim == 128, page_size == 16
+ * Errors: HMA_EINVAL (NULL pointer with n_pages > 0, negative count,
+ * misalignment, stride smaller than needed to keep pools apart),
+ * HMA_EUNSUPPORTED (head_dim / page_size), HMA_EHIP.
+ */
+HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst_bf16,
+                           const int32_t *src_pages, const int32_t *dst_pages, int32_t n_pages,
+                           int32_t n_pools, int64_t src_pool_stride_pages,
+                           int64_t dst_pool_stride_pages, int32_t num_kv_heads,
+                           int32_t head_dim, int32_t page_size, void *stream);
+
+/*
+ * hma_decode_attn_bfp8 -- single-token GQA decode attention over the paged,
+ * mixed-format KV cache, with BFP8 pages decoded in registers inside the
+ * paged read (Sec. 3.3, Fig. 2: reconstruction inline in paged attention).
+ *
+ * For sequence b and query head h (kv head j = h / (num_q_heads / num_kv_heads)):
+ *   s_t = scale * <q[b][h], k_t>  for logical tokens t in [0, context_lens[b])
+ *   out[b][h] = sum_t softmax(s)_t v_t           (BF16, round to nearest even)
+ *   lse[b][h] = log(sum_t exp(s_t))              (natural log, float32)
+ * k_t and v_t are the exact values of the stored BFP8 elements (or the stored
+ * BF16 values of tagged pages).  Products and sums use float32; the context
+ * is split into ranges of tokens_per_split tokens handled by separate
+ * workgroups whose partial (max, sum, weighted values) are merged exactly by
+ * log-sum-exp.  context_lens[b] == 0 gives out = 0 and lse = -inf.  Slots at
+ * or past the context end in the last page are never used, whatever they
+ * hold.
+ *
+ *   q          uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
+ *   k_mant, v_mant  uint8 mantissa pools, 16-byte aligned
+ *   k_exp, v_exp    uint8 exponent pools, 16-byte aligned
+ *   k_bf16, v_bf16  uint16 BF16 pools, 16-byte aligned; may be NULL when no
+ *              page-table entry carries HMA_PAGE_BF16
+ *   page_table int32 [batch][max_pages_per_seq]
+ *   context_lens  int32 [batch], each in [0, max_context_len]
+ *   max_context_len  host-side bound that sizes the launch (no device read
+ *              on the host); must be <= max_pages_per_seq * page_size
+ *   num_q_heads % num_kv_heads == 0 and num_q_heads / num_kv_heads <= 16;
+ *   head_dim == 128, page_size == 16
+ *   scale      softmax scale (typically 1/sqrt(128))
+ *   tokens_per_split  0 = chosen by the library (see
+ *              hma_decode_attn_tokens_per_split); else a positive multiple
+ *              of 32
+ *   out        uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
+ *   lse        float32 [batch][num_q_heads], or NULL
+ *   workspace  device buffer of at least hma_decode_attn_workspace_bytes()
+ *              bytes for the same (batch, heads, max_context_len,
+ *              tokens_per_split), 256-byte aligned, zero-filled once by the
+ *              caller when allocated; every call leaves it ready for the
+ *              next one.  May be NULL when the required size is 0.
+ * Errors: HMA_EINVAL, HMA_EUNSUPPORTED, HMA_EWORKSPACE, HMA_EHIP.
+ */
+HMA_API int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
+                         const uint8_t *v_mant, const uint8_t *v_exp, const uint16_t *k_bf16,
+                         const uint16_t *v_bf16, const int32_t *page_table,
+                         int32_t max_pages_per_seq, const int32_t *context_lens,
+                         int32_t max_context_len, int32_t batch, int32_t num_q_heads,
+                         int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
+                         int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
+                         size_t workspace_bytes, void *stream);
+
+/*
+ * Split length the library uses for tokens_per_split = 0 (host only, no HIP
+ * call).  Returns a positive multiple of 32, or 0 on invalid sizes.
+ */
+HMA_API int32_t hma_decode_attn_tokens_per_split(int32_t batch, int32_t num_q_heads,
+                                         int32_t num_kv_heads, int32_t max_context_len);
+
+/*
+ * Workspace bytes hma_decode_attn_bfp8 needs for these sizes (host only).
+ * tokens_per_split = 0 means the library's choice.  Returns 0 when no
+ * workspace is needed (every sequence fits one split) and (size_t)-1 on
+ * invalid sizes.
+ */
+HMA_API size_t hma_decode_attn_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t max_context_len, int32_t tokens_per_split);
+
+/* Static, never-NULL description of a status code. */
+HMA_API const char *hma_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HMA_H */

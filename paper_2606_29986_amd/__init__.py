@@ -1,0 +1,158 @@
+"""paper_2606_29986_amd -- MI355X (gfx950) deferred-dequantization decode path.
+
+Thin Python binding over ``libhma.so`` (C ABI in ``include/hma.h``): argument
+marshalling only.  Every step of the path runs in the library's HIP kernels;
+torch supplies device memory and the current HIP stream.  If the library is
+missing the import still succeeds but every call raises -- there is no
+fallback of any kind.
+
+Paper: "HBM Is Not All You Need" (HMA-Serve), arXiv 2606.29986, Sec. 3.3.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhma.so")
+
+HMA_OK = 0
+HMA_EINVAL = -1
+HMA_EUNSUPPORTED = -2
+HMA_EWORKSPACE = -3
+HMA_EHIP = -4
+PAGE_BF16 = 0x40000000
+PAGE_ID_MASK = 0x3FFFFFFF
+HEAD_DIM = 128
+PAGE_SIZE = 16
+
+_lib = None
+
+
+class HmaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhma.so; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libhma.so not built at {LIB_PATH}; run "
+                           "`python -m paper_2606_29986_amd.build` (no fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    L.hma_bfp8_dequant_pages.argtypes = [vp, vp, vp, vp, vp, i32, i32, i64, i64, i32, i32, i32, vp]
+    L.hma_bfp8_dequant_pages.restype = ctypes.c_int
+    L.hma_decode_attn_bfp8.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, i32,
+                                       i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, sz, vp]
+    L.hma_decode_attn_bfp8.restype = ctypes.c_int
+    L.hma_decode_attn_tokens_per_split.argtypes = [i32, i32, i32, i32]
+    L.hma_decode_attn_tokens_per_split.restype = i32
+    L.hma_decode_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+    L.hma_decode_attn_workspace_bytes.restype = sz
+    L.hma_status_string.argtypes = [ctypes.c_int]
+    L.hma_status_string.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().hma_status_string(int(status)).decode()
+
+
+def _ptr(t):
+    """Device pointer of a torch tensor (or None -> NULL).  Raw ints pass through."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check_dev(*ts):
+    for t in ts:
+        if t is not None and not isinstance(t, int):
+            if not t.is_cuda:
+                raise ValueError("libhma takes device tensors only")
+            if not t.is_contiguous():
+                raise ValueError("libhma takes contiguous tensors only")
+
+
+def tokens_per_split(batch: int, num_q_heads: int, num_kv_heads: int, max_context_len: int) -> int:
+    """Split length the library picks when tokens_per_split = 0."""
+    return int(lib().hma_decode_attn_tokens_per_split(batch, num_q_heads, num_kv_heads,
+                                                      max_context_len))
+
+
+def workspace_bytes(batch: int, num_q_heads: int, num_kv_heads: int, max_context_len: int,
+                    tokens_per_split: int = 0) -> int:
+    n = int(lib().hma_decode_attn_workspace_bytes(batch, num_q_heads, num_kv_heads,
+                                                  max_context_len, tokens_per_split))
+    if n == (1 << 64) - 1:
+        raise HmaError(HMA_EINVAL, "hma_decode_attn_workspace_bytes")
+    return n
+
+
+def alloc_workspace(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split=0,
+                    device="cuda"):
+    """Zero-filled workspace tensor of the size the library needs (or None)."""
+    import torch
+    n = workspace_bytes(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split)
+    if n == 0:
+        return None
+    return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pools=1,
+                       src_pool_stride_pages=0, dst_pool_stride_pages=0, num_kv_heads=8,
+                       head_dim=HEAD_DIM, page_size=PAGE_SIZE, stream=None) -> None:
+    """hma_bfp8_dequant_pages: rebuild BFP8 pages into the BF16 pool dst_bf16.
+
+    src_mant uint8, src_exp uint8, dst_bf16 int16/uint16/bfloat16 device
+    tensors; src_pages / dst_pages int32 device tensors of equal length."""
+    _check_dev(src_mant, src_exp, dst_bf16, src_pages, dst_pages)
+    n = int(src_pages.numel()) if not isinstance(src_pages, int) else None
+    if n is None or int(dst_pages.numel()) != n:
+        raise ValueError("src_pages and dst_pages must be tensors of equal length")
+    rc = lib().hma_bfp8_dequant_pages(_ptr(src_mant), _ptr(src_exp), _ptr(dst_bf16),
+                                      _ptr(src_pages), _ptr(dst_pages), n, n_pools,
+                                      src_pool_stride_pages, dst_pool_stride_pages, num_kv_heads,
+                                      head_dim, page_size, _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_bfp8_dequant_pages")
+
+
+def decode_attn_bfp8(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len,
+                     out, k_bf16=None, v_bf16=None, lse=None, scale=None, num_kv_heads=None,
+                     tokens_per_split=0, workspace=None, head_dim=HEAD_DIM, page_size=PAGE_SIZE,
+                     stream=None) -> None:
+    """hma_decode_attn_bfp8: fused BFP8 paged decode attention into ``out``.
+
+    q, out: [B][Hq][128] 16-bit tensors (BF16 bits); pools as in hma.h;
+    page_table int32 [B][max_pages]; context_lens int32 [B];
+    max_context_len: host int bound.  num_kv_heads defaults to k_mant.shape[1]."""
+    _check_dev(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, out, k_bf16, v_bf16,
+               lse, workspace)
+    B, Hq, D = q.shape
+    hkv = int(num_kv_heads if num_kv_heads is not None else k_mant.shape[1])
+    if scale is None:
+        scale = 1.0 / (D ** 0.5)
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    rc = lib().hma_decode_attn_bfp8(
+        _ptr(q), _ptr(k_mant), _ptr(k_exp), _ptr(v_mant), _ptr(v_exp), _ptr(k_bf16),
+        _ptr(v_bf16), _ptr(page_table), int(page_table.shape[1]), _ptr(context_lens),
+        int(max_context_len), B, Hq, hkv, D, page_size, float(scale), int(tokens_per_split),
+        _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_decode_attn_bfp8")

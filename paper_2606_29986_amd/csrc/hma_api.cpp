@@ -1,0 +1,197 @@
+// hma_api.cpp -- the exported C ABI of libhma (declared in include/hma.h).
+//
+// Every argument is validated on the host before any HIP call, so a rejected
+// call enqueues nothing and the checks can run on a machine without a GPU.
+#include "hma.h"
+
+#include <limits.h>
+#include <stdint.h>
+
+#include "hma_internal.h"
+
+namespace {
+
+constexpr int32_t kSupportedHeadDim = 128;
+constexpr int32_t kSupportedPageSize = 16;
+constexpr int32_t kMaxGroup = 16;            // query heads per KV head (MFMA N = 16)
+constexpr int32_t kSplitQuantum = 32;        // tokens per attention step
+constexpr int64_t kTargetWorkgroups = 2048;  // auto split: aim for ~8 workgroups per CU
+constexpr int32_t kMinAutoSplit = 512;
+constexpr int32_t kMaxAutoSplit = 1024;
+
+bool aligned(const void *p, uintptr_t a)
+{
+    return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+int32_t round_up(int64_t x, int32_t q)
+{
+    return (int32_t)(((x + q - 1) / q) * q);
+}
+
+bool attn_sizes_ok(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx)
+{
+    return batch >= 0 && hq > 0 && hkv > 0 && hq % hkv == 0 && max_ctx >= 0;
+}
+
+int32_t auto_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx)
+{
+    const int64_t pairs = (int64_t)batch * hkv;
+    const int32_t whole = round_up(max_ctx > 0 ? max_ctx : 1, kSplitQuantum);
+    int64_t tps = (pairs * (int64_t)max_ctx + kTargetWorkgroups - 1) / kTargetWorkgroups;
+    tps = round_up(tps, 256);
+    if (tps < kMinAutoSplit)
+        tps = kMinAutoSplit;
+    if (tps > kMaxAutoSplit)
+        tps = kMaxAutoSplit;
+    if (tps > whole)
+        tps = whole;
+    return (int32_t)tps;
+}
+
+int32_t splits_for(int32_t max_ctx, int32_t tps)
+{
+    return max_ctx <= 0 ? 1 : (int32_t)(((int64_t)max_ctx + tps - 1) / tps);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hma_status_string(int status)
+{
+    switch (status) {
+    case HMA_OK:
+        return "ok";
+    case HMA_EINVAL:
+        return "invalid argument (null pointer, bad size, misalignment or aliasing)";
+    case HMA_EUNSUPPORTED:
+        return "unsupported configuration (head_dim must be 128, page_size 16, "
+               "query heads per KV head at most 16)";
+    case HMA_EWORKSPACE:
+        return "workspace missing or too small";
+    case HMA_EHIP:
+        return "HIP kernel launch failed";
+    default:
+        return "unknown status";
+    }
+}
+
+int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst_bf16,
+                           const int32_t *src_pages, const int32_t *dst_pages, int32_t n_pages,
+                           int32_t n_pools, int64_t src_pool_stride_pages,
+                           int64_t dst_pool_stride_pages, int32_t num_kv_heads,
+                           int32_t head_dim, int32_t page_size, void *stream)
+{
+    if (n_pages < 0 || n_pools < 0 || num_kv_heads <= 0)
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (n_pages == 0 || n_pools == 0)
+        return HMA_OK;
+    if (!src_mant || !src_exp || !dst_bf16 || !src_pages || !dst_pages)
+        return HMA_EINVAL;
+    if (!aligned(src_mant, 16) || !aligned(src_exp, 16) || !aligned(dst_bf16, 16))
+        return HMA_EINVAL;
+    if ((const void *)dst_bf16 == (const void *)src_mant || (const void *)dst_bf16 == (const void *)src_exp)
+        return HMA_EINVAL;
+    if (n_pools > 1 && (src_pool_stride_pages < 1 || dst_pool_stride_pages < 1))
+        return HMA_EINVAL;
+    if (src_pool_stride_pages < 0 || dst_pool_stride_pages < 0)
+        return HMA_EINVAL;
+    const int64_t tiles = (int64_t)n_pools * n_pages * num_kv_heads;
+    if (tiles / 4 + 1 > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    const int rc = hma::launch_bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages,
+                                                  n_pages, n_pools, src_pool_stride_pages,
+                                                  dst_pool_stride_pages, num_kv_heads,
+                                                  static_cast<hipStream_t>(stream));
+    return rc == 0 ? HMA_OK : HMA_EHIP;
+}
+
+int32_t hma_decode_attn_tokens_per_split(int32_t batch, int32_t num_q_heads,
+                                         int32_t num_kv_heads, int32_t max_context_len)
+{
+    if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
+        return 0;
+    return auto_tokens_per_split(batch, num_kv_heads, max_context_len);
+}
+
+size_t hma_decode_attn_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                       int32_t max_context_len, int32_t tokens_per_split)
+{
+    if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
+        return (size_t)-1;
+    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0)
+        return (size_t)-1;
+    const int32_t tps = tokens_per_split ? tokens_per_split
+                                         : auto_tokens_per_split(batch, num_kv_heads, max_context_len);
+    return hma::attn_workspace_bytes(batch, num_q_heads, num_kv_heads, splits_for(max_context_len, tps));
+}
+
+int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
+                         const uint8_t *v_mant, const uint8_t *v_exp, const uint16_t *k_bf16,
+                         const uint16_t *v_bf16, const int32_t *page_table,
+                         int32_t max_pages_per_seq, const int32_t *context_lens,
+                         int32_t max_context_len, int32_t batch, int32_t num_q_heads,
+                         int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
+                         int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
+                         size_t workspace_bytes, void *stream)
+{
+    if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (num_q_heads / num_kv_heads > kMaxGroup)
+        return HMA_EUNSUPPORTED;
+    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0)
+        return HMA_EINVAL;
+    if (max_pages_per_seq < 0 || (int64_t)max_context_len > (int64_t)max_pages_per_seq * page_size)
+        return HMA_EINVAL;
+    if (!(scale == scale))
+        return HMA_EINVAL;
+    if (batch == 0)
+        return HMA_OK;
+    if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !page_table || !context_lens || !out)
+        return HMA_EINVAL;
+    if ((k_bf16 == nullptr) != (v_bf16 == nullptr))
+        return HMA_EINVAL;
+    if (!aligned(q, 16) || !aligned(out, 16) || !aligned(k_mant, 16) || !aligned(v_mant, 16) ||
+        !aligned(k_exp, 16) || !aligned(v_exp, 16) || !aligned(k_bf16, 16) || !aligned(v_bf16, 16) ||
+        !aligned(lse, 4))
+        return HMA_EINVAL;
+    const int32_t tps = tokens_per_split ? tokens_per_split
+                                         : auto_tokens_per_split(batch, num_kv_heads, max_context_len);
+    const int32_t n_splits = splits_for(max_context_len, tps);
+    if ((int64_t)batch * num_kv_heads * n_splits > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    const size_t need = hma::attn_workspace_bytes(batch, num_q_heads, num_kv_heads, n_splits);
+    if (need > 0 && (workspace == nullptr || workspace_bytes < need))
+        return HMA_EWORKSPACE;
+    if (need > 0 && !aligned(workspace, 256))
+        return HMA_EINVAL;
+
+    hma::AttnLaunch a;
+    a.q = q;
+    a.k_mant = k_mant;
+    a.k_exp = k_exp;
+    a.v_mant = v_mant;
+    a.v_exp = v_exp;
+    a.k_bf16 = k_bf16;
+    a.v_bf16 = v_bf16;
+    a.page_table = page_table;
+    a.ctx_lens = context_lens;
+    a.out = out;
+    a.lse = lse;
+    a.workspace = workspace;
+    a.max_pages = max_pages_per_seq;
+    a.batch = batch;
+    a.hq = num_q_heads;
+    a.hkv = num_kv_heads;
+    a.tps = tps;
+    a.n_splits = n_splits;
+    a.scale = scale;
+    return hma::launch_decode_attn(a, static_cast<hipStream_t>(stream)) == 0 ? HMA_OK : HMA_EHIP;
+}
+
+}  // extern "C"

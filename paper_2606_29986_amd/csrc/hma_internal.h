@@ -1,0 +1,36 @@
+// hma_internal.h -- launchers behind the C ABI (not exported).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hma {
+
+// Returns 0 on a successful launch, -1 if the launch failed.
+int launch_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst,
+                              const int32_t *src_pages, const int32_t *dst_pages,
+                              int32_t n_pages, int32_t n_pools, int64_t src_stride_pages,
+                              int64_t dst_stride_pages, int32_t hkv, hipStream_t stream);
+
+struct AttnLaunch {
+    const uint16_t *q;
+    const uint8_t *k_mant, *k_exp, *v_mant, *v_exp;
+    const uint16_t *k_bf16, *v_bf16;
+    const int32_t *page_table;
+    const int32_t *ctx_lens;
+    uint16_t *out;
+    float *lse;
+    void *workspace;
+    int32_t max_pages, batch, hq, hkv, tps, n_splits;
+    float scale;
+};
+
+// Workspace layout for n_splits > 1: tickets int32 [B*Hkv] (256-byte padded),
+// then (max, sum) float2 [B*Hkv][n_splits][g], then values float
+// [B*Hkv][n_splits][g][128].
+size_t attn_workspace_bytes(int32_t batch, int32_t hq, int32_t hkv, int32_t n_splits);
+
+int launch_decode_attn(const AttnLaunch &a, hipStream_t stream);
+
+}  // namespace hma

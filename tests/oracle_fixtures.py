@@ -33,20 +33,34 @@ class PagedKV:
 
 
 def make_paged(w: wl.Workload, layer: int = 0, ctx=None, bf16_fraction: float = 0.0,
-               garbage_tail: bool = True, with_bf16_pool: bool = True) -> PagedKV:
+               garbage_tail: bool = True, with_bf16_pool: bool = True,
+               value_seqs=None) -> PagedKV:
     """Build one layer of workload w with the oracle's encoder.
 
     ctx overrides the workload's length draw.  bf16_fraction of the pages
     (seeded) are tagged as BF16 pages whose BF16 pool holds the exact decoded
     values.  garbage_tail fills the slots past each sequence's end with random
-    bytes that no result may depend on."""
+    bytes that no result may depend on.  value_seqs (for the very large
+    workloads) restricts the value draws to the pages of those sequences;
+    every other page holds zeros, and only those sequences may be checked."""
     ctx = wl.context_lens(w) if ctx is None else np.asarray(ctx, dtype=np.int32)
     pt, total = wl.page_table(w, ctx)
     total = max(total, 1)
-    k = wl.kv_values_bf16(w, layer, "k", total)
-    v = wl.kv_values_bf16(w, layer, "v", total)
-    k_mant, k_exp = oracle.encode_blocks(k)
-    v_mant, v_exp = oracle.encode_blocks(v)
+    if value_seqs is None:
+        k_mant, k_exp = oracle.encode_blocks(wl.kv_values_bf16(w, layer, "k", total))
+        v_mant, v_exp = oracle.encode_blocks(wl.kv_values_bf16(w, layer, "v", total))
+    else:
+        npg_all = wl.pages_per_seq(ctx, w.page_size)
+        ids = np.concatenate([pt[b, :npg_all[b]] for b in value_seqs]).astype(np.int64)
+        shape = (total, w.num_kv_heads, w.page_size, w.head_dim)
+        k_mant = np.zeros(shape, np.uint8)
+        v_mant = np.zeros(shape, np.uint8)
+        k_exp = np.zeros(shape[:-1] + (w.head_dim // 16,), np.uint8)
+        v_exp = np.zeros_like(k_exp)
+        for kind, mant, ex in (("k", k_mant, k_exp), ("v", v_mant, v_exp)):
+            m_sub, e_sub = oracle.encode_blocks(wl.kv_values_bf16(w, layer, kind, ids.size))
+            mant[ids] = m_sub
+            ex[ids] = e_sub
     if garbage_tail:
         npg = wl.pages_per_seq(ctx, w.page_size)
         salt = 0

@@ -1,0 +1,137 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/hma.h declares, and rejects bad arguments on the host before any HIP
+call (so nothing is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_29986_amd as hma
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hma.h")
+
+# a non-NULL, 256-byte aligned fake device address: never dereferenced because
+# every call below fails validation before any HIP call
+FAKE = 0x10000
+MISALIGNED = 0x10008
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"HMA_API\s+[\w\s\*]+?\b(hma_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    assert names == sorted(["hma_bfp8_dequant_pages", "hma_decode_attn_bfp8",
+                            "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
+                            "hma_status_string"])
+
+
+def test_library_exports_every_declared_symbol():
+    L = hma.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    # nothing but the C ABI is exported
+    out = os.popen(f"nm -D --defined-only {hma.LIB_PATH}").read()
+    exported = sorted(l.split()[-1] for l in out.splitlines() if " T " in l)
+    assert exported == declared_functions()
+
+
+def test_status_strings():
+    for st in (0, -1, -2, -3, -4, 7):
+        s = hma.status_string(st)
+        assert isinstance(s, str) and s
+    assert hma.status_string(0) == "ok"
+
+
+def test_split_and_workspace_queries():
+    tps = hma.tokens_per_split(16, 64, 8, 8192)
+    assert tps > 0 and tps % 32 == 0
+    S = -(-8192 // tps)
+    ws = hma.workspace_bytes(16, 64, 8, 8192)
+    pairs, g = 16 * 8, 8
+    tickets = (pairs * 4 + 255) // 256 * 256
+    ml = (pairs * S * g * 8 + 255) // 256 * 256
+    assert ws == tickets + ml + pairs * S * g * 128 * 4
+    # one split: no workspace
+    assert hma.workspace_bytes(4, 32, 8, 512, 512) == 0
+    assert hma.workspace_bytes(4, 32, 8, 0) == 0
+    # explicit split sizes must be multiples of 32
+    with pytest.raises(hma.HmaError):
+        hma.workspace_bytes(4, 32, 8, 512, 48)
+    with pytest.raises(hma.HmaError):
+        hma.workspace_bytes(4, 30, 8, 512)
+    assert hma.tokens_per_split(4, 30, 8, 512) == 0
+
+
+def _dequant(**kw):
+    a = dict(src_mant=FAKE, src_exp=FAKE, dst=FAKE * 2, src_pages=FAKE, dst_pages=FAKE,
+             n_pages=4, n_pools=1, src_stride=0, dst_stride=0, hkv=8, D=128, P=16)
+    a.update(kw)
+    return hma.lib().hma_bfp8_dequant_pages(a["src_mant"], a["src_exp"], a["dst"], a["src_pages"],
+                                            a["dst_pages"], a["n_pages"], a["n_pools"],
+                                            a["src_stride"], a["dst_stride"], a["hkv"], a["D"],
+                                            a["P"], None)
+
+
+def test_dequant_validation():
+    assert _dequant(n_pages=0) == hma.HMA_OK             # no-op, nothing touched
+    assert _dequant(n_pools=0) == hma.HMA_OK
+    assert _dequant(n_pages=-1) == hma.HMA_EINVAL
+    assert _dequant(hkv=0) == hma.HMA_EINVAL
+    assert _dequant(D=64) == hma.HMA_EUNSUPPORTED
+    assert _dequant(P=32) == hma.HMA_EUNSUPPORTED
+    for k in ("src_mant", "src_exp", "dst", "src_pages", "dst_pages"):
+        assert _dequant(**{k: None}) == hma.HMA_EINVAL, k
+    for k in ("src_mant", "src_exp", "dst"):
+        assert _dequant(**{k: MISALIGNED}) == hma.HMA_EINVAL, k
+    assert _dequant(dst=FAKE) == hma.HMA_EINVAL           # aliases the source
+    assert _dequant(n_pools=2, src_stride=0, dst_stride=4) == hma.HMA_EINVAL
+    assert _dequant(n_pools=2, src_stride=4, dst_stride=-1) == hma.HMA_EINVAL
+
+
+def _attn(**kw):
+    a = dict(q=FAKE, km=FAKE, ke=FAKE, vm=FAKE, ve=FAKE, kb=None, vb=None, pt=FAKE, maxp=512,
+             ctx=FAKE, maxctx=8192, B=16, Hq=64, Hkv=8, D=128, P=16, scale=0.088388346,
+             tps=0, out=FAKE, lse=None, ws=None, wsb=0)
+    a.update(kw)
+    return hma.lib().hma_decode_attn_bfp8(a["q"], a["km"], a["ke"], a["vm"], a["ve"], a["kb"],
+                                          a["vb"], a["pt"], a["maxp"], a["ctx"], a["maxctx"],
+                                          a["B"], a["Hq"], a["Hkv"], a["D"], a["P"], a["scale"],
+                                          a["tps"], a["out"], a["lse"], a["ws"], a["wsb"], None)
+
+
+def test_attn_validation():
+    need = hma.workspace_bytes(16, 64, 8, 8192)
+    assert need > 0
+    # everything valid except the missing workspace
+    assert _attn() == hma.HMA_EWORKSPACE
+    assert _attn(ws=FAKE, wsb=need - 1) == hma.HMA_EWORKSPACE
+    assert _attn(ws=MISALIGNED, wsb=need) == hma.HMA_EINVAL
+    assert _attn(Hq=60) == hma.HMA_EINVAL                  # Hq % Hkv != 0
+    assert _attn(Hq=8 * 17) == hma.HMA_EUNSUPPORTED        # group of 17
+    assert _attn(D=64) == hma.HMA_EUNSUPPORTED
+    assert _attn(P=32) == hma.HMA_EUNSUPPORTED
+    assert _attn(tps=48) == hma.HMA_EINVAL
+    assert _attn(tps=-32) == hma.HMA_EINVAL
+    assert _attn(maxctx=-1) == hma.HMA_EINVAL
+    assert _attn(maxp=100) == hma.HMA_EINVAL               # 8192 tokens need 512 pages
+    assert _attn(scale=float("nan")) == hma.HMA_EINVAL
+    assert _attn(B=0) == hma.HMA_OK                        # nothing to do
+    for k in ("q", "km", "ke", "vm", "ve", "pt", "ctx", "out"):
+        assert _attn(**{k: None}) == hma.HMA_EINVAL, k
+    for k in ("q", "km", "ke", "vm", "ve", "out"):
+        assert _attn(**{k: MISALIGNED}) == hma.HMA_EINVAL, k
+    assert _attn(kb=FAKE, vb=None) == hma.HMA_EINVAL       # both BF16 pools or neither
+    assert _attn(kb=MISALIGNED, vb=FAKE) == hma.HMA_EINVAL
+    assert _attn(lse=0x10002) == hma.HMA_EINVAL
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(hma, "_lib", None)
+    monkeypatch.setattr(hma, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        hma.lib()

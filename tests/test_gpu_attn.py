@@ -1,0 +1,197 @@
+"""GPU parity of hma_decode_attn_bfp8 against the float64 oracle.
+
+Paper: decode attention reads raw BFP8 pages and rebuilds them inline in the
+paged-attention kernel (Sec. 3.3, Fig. 2).  Bar: |gpu - oracle| <= 2e-3 +
+1e-2 |oracle| elementwise on the BF16 output, plus exact-equality invariants
+(single token, page placement, page format, GQA, split count, repeat runs)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_29986_amd as hma
+import workloads as wl
+from gpu_util import LSE_ATOL, LSE_RTOL, DevKV, assert_attn_close, bf16_bits_to_f64, dev, note
+from oracle_fixtures import PagedKV, make_paged, tiny_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def test_smoke_workload_matches_oracle():
+    w = wl.WORKLOADS[0]
+    note(f"attn: {w.name} full, auto split")
+    kv = make_paged(w)
+    ref, ref_lse = kv.oracle_attn()
+    d = DevKV(kv)
+    out, lse = d.attn()
+    assert_attn_close(out, lse, ref, ref_lse, what=w.name)
+
+
+@pytest.mark.parametrize("tps", [32, 64, 96, 256, 0])
+def test_ragged_with_garbage_tails_and_splits(tps):
+    w = tiny_workload(Hq=32, Hkv=8, B=9, index=0)
+    ctx = [0, 1, 15, 16, 17, 31, 33, 300, 511]
+    note(f"attn: ragged ctx={ctx} tps={tps}")
+    kv = make_paged(w, ctx=ctx, garbage_tail=True)
+    ref, ref_lse = kv.oracle_attn()
+    out, lse = DevKV(kv).attn(tokens_per_split=tps)
+    assert_attn_close(out, lse, ref, ref_lse, what=f"ragged tps={tps}")
+    got = bf16_bits_to_f64(out)
+    assert not got[0].any() and np.isneginf(lse[0].cpu().numpy()).all()
+
+
+@pytest.mark.parametrize("group", [1, 2, 4, 5, 8, 16])
+def test_group_sizes(group):
+    w = tiny_workload(Hq=2 * group, Hkv=2, B=3, index=1)
+    ctx = [70, 129, 200]
+    note(f"attn: group {group} ctx={ctx}")
+    kv = make_paged(w, ctx=ctx)
+    ref, ref_lse = kv.oracle_attn()
+    for tps in (64, 0):
+        out, lse = DevKV(kv).attn(tokens_per_split=tps)
+        assert_attn_close(out, lse, ref, ref_lse, what=f"g={group} tps={tps}")
+
+
+def test_single_token_is_v0_exactly():
+    """ctx = 1: the softmax weight is exactly 1, so the BF16 output must equal
+    the decoded v_0 bit for bit (pins the in-register decode of V), and the
+    lse equals the single score."""
+    w = tiny_workload(Hq=16, Hkv=2, B=5, index=2)
+    note("attn: single-token contexts")
+    kv = make_paged(w, ctx=[1] * 5)
+    # make the V rows of the first tokens cover extreme exponents, incl. BF16 subnormals
+    for b, E in zip(range(5), (0, 3, 100, 127, 200)):
+        pid = kv.page_table[b, 0]
+        kv.v_exp[pid, :, 0, :] = E
+    kv.k_bf16 = oracle.decode_blocks(kv.k_mant, kv.k_exp)
+    kv.v_bf16 = oracle.decode_blocks(kv.v_mant, kv.v_exp)
+    ref, ref_lse = kv.oracle_attn()
+    out, lse = DevKV(kv).attn()
+    got = out.cpu().numpy().view(np.uint16)
+    for b in range(5):
+        pid = kv.page_table[b, 0]
+        for h in range(16):
+            want = kv.v_bf16[pid, h // 8, 0]
+            assert np.array_equal(got[b, h], want), (b, h)
+    np.testing.assert_allclose(lse.cpu().numpy(), ref_lse, rtol=LSE_RTOL, atol=LSE_ATOL)
+
+
+def test_page_placement_invariance_bitwise():
+    w = tiny_workload(Hq=32, Hkv=8, B=4, index=3)
+    ctx = [100, 257, 64, 480]
+    note("attn: physical page placement")
+    kv = make_paged(w, ctx=ctx)
+    out1, lse1 = DevKV(kv).attn(tokens_per_split=64)
+    n = kv.k_mant.shape[0]
+    perm = np.random.default_rng(4).permutation(n)
+    inv = np.argsort(perm)
+    kv2 = PagedKV(kv.q, *(np.ascontiguousarray(a[inv]) for a in
+                          (kv.k_mant, kv.k_exp, kv.v_mant, kv.v_exp, kv.k_bf16, kv.v_bf16)),
+                  perm[kv.page_table].astype(np.int32), kv.ctx, kv.num_kv_heads, kv.page_size,
+                  kv.scale)
+    out2, lse2 = DevKV(kv2).attn(tokens_per_split=64)
+    assert torch.equal(out1, out2) and torch.equal(lse1, lse2)
+
+
+def test_bf16_pages_equal_bfp8_pages_bitwise():
+    """Pages tagged BF16 holding the decoded values give the same output as
+    the BFP8 pages, bit for bit; and after hma_bfp8_dequant_pages rebuilds
+    every page into the BF16 pool, an all-BF16 page table matches too."""
+    w = wl.WORKLOADS[0]
+    note("attn: mixed BF16/BFP8 pages")
+    a = make_paged(w, bf16_fraction=0.0)
+    b = make_paged(w, bf16_fraction=0.5)
+    out_a, lse_a = DevKV(a).attn(use_bf16_pools=False)
+    out_b, lse_b = DevKV(b).attn()
+    assert torch.equal(out_a, out_b) and torch.equal(lse_a, lse_b)
+    # rebuild all pages on the GPU, then read everything from the BF16 pool
+    d = DevKV(a)
+    n = a.k_mant.shape[0]
+    ids = dev(np.arange(n, dtype=np.int32))
+    kb = torch.empty((n, 8, 16, 128), dtype=torch.int16, device="cuda")
+    vb = torch.empty_like(kb)
+    hma.bfp8_dequant_pages(d.k_mant, d.k_exp, kb, ids, ids, num_kv_heads=8)
+    hma.bfp8_dequant_pages(d.v_mant, d.v_exp, vb, ids, ids, num_kv_heads=8)
+    d.k_bf16, d.v_bf16 = kb, vb
+    d.pt = dev(a.page_table | wl.TAG_BF16)
+    out_c, lse_c = d.attn()
+    assert torch.equal(out_a, out_c) and torch.equal(lse_a, lse_c)
+
+
+def test_gqa_identical_queries_bitwise():
+    w = tiny_workload(Hq=32, Hkv=4, B=2, index=4)
+    note("attn: identical queries within a group")
+    kv = make_paged(w, ctx=[200, 333])
+    for j in range(4):
+        kv.q[:, 8 * j + 1: 8 * j + 8] = kv.q[:, 8 * j: 8 * j + 1]
+    out, _ = DevKV(kv).attn(tokens_per_split=64)
+    o = out.cpu().numpy()
+    for j in range(4):
+        for h in range(8 * j + 1, 8 * j + 8):
+            assert np.array_equal(o[:, h], o[:, 8 * j])
+    assert not np.array_equal(o[:, 0], o[:, 8])
+
+
+def test_split_count_invariance_and_determinism():
+    w = tiny_workload(Hq=64, Hkv=8, B=3, index=5)
+    ctx = [1000, 777, 1500]
+    note(f"attn: split invariance ctx={ctx}")
+    kv = make_paged(w, ctx=ctx)
+    ref, ref_lse = kv.oracle_attn()
+    d = DevKV(kv)
+    first = None
+    for tps in (32, 128, 512, 1024, 1504):
+        out, lse = d.attn(tokens_per_split=tps)
+        assert_attn_close(out, lse, ref, ref_lse, what=f"tps={tps}")
+        again, lse2 = d.attn(tokens_per_split=tps)
+        assert torch.equal(out, again) and torch.equal(lse, lse2), f"tps={tps} not deterministic"
+        first = out if first is None else first
+
+
+def test_all_equal_keys_uniform_average():
+    w = tiny_workload(Hq=8, Hkv=1, B=1, index=6)
+    note("attn: all keys equal")
+    kv = make_paged(w, ctx=[300])
+    kv.k_mant[:] = kv.k_mant[kv.page_table[0, 0], 0, 0]
+    kv.k_exp[:] = kv.k_exp[kv.page_table[0, 0], 0, 0]
+    ref, ref_lse = kv.oracle_attn()
+    vmean = np.stack([oracle.bf16_to_f64(oracle.decode_blocks(
+        kv.v_mant[kv.page_table[0, t // 16], 0, t % 16], kv.v_exp[kv.page_table[0, t // 16], 0, t % 16]))
+        for t in range(300)]).mean(axis=0)
+    np.testing.assert_allclose(ref[0], np.broadcast_to(vmean, ref[0].shape), atol=1e-12)
+    out, lse = DevKV(kv).attn(tokens_per_split=64)
+    assert_attn_close(out, lse, ref, ref_lse, what="uniform")
+
+
+# ---------------------------------------------------------- full-size cases
+
+def _sample_seqs(w, n_seq, seed):
+    r = np.random.default_rng(seed)
+    return np.sort(r.choice(w.batch, size=min(n_seq, w.batch), replace=False))
+
+
+def _oracle_rows(kv, seqs):
+    """Oracle on a subset of sequences (the oracle's cost grows with context)."""
+    sub = PagedKV(np.ascontiguousarray(kv.q[seqs]), kv.k_mant, kv.k_exp, kv.v_mant, kv.v_exp,
+                  kv.k_bf16, kv.v_bf16, np.ascontiguousarray(kv.page_table[seqs]),
+                  np.ascontiguousarray(kv.ctx[seqs]), kv.num_kv_heads, kv.page_size, kv.scale)
+    return sub.oracle_attn()
+
+
+@pytest.mark.parametrize("index,n_seq", [(1, 6), (2, 10), (3, 4), (4, 12)])
+def test_full_size_workload_sampled(index, n_seq):
+    """One layer of each evaluated workload at its full size, launched exactly
+    as the benchmark launches it (automatic split); the oracle checks a
+    seeded sample of whole sequences (every head, every channel).  For the
+    200-sequence trace mix only the sampled sequences' pages carry drawn
+    values (the rest are zeros) to keep the host-side draw short."""
+    w = wl.WORKLOADS[index]
+    note(f"attn: full-size {w.name}")
+    seqs = _sample_seqs(w, n_seq, seed=index)
+    kv = make_paged(w, bf16_fraction=w.bf16_page_fraction,
+                    with_bf16_pool=w.bf16_page_fraction > 0,
+                    value_seqs=seqs if index == 4 else None)
+    out, lse = DevKV(kv).attn()
+    ref, ref_lse = _oracle_rows(kv, seqs)
+    err = assert_attn_close(out, lse, ref, ref_lse, rows=seqs, what=w.name)
+    note(f"attn: {w.name} max abs err {err:.3g} on {len(seqs)} sequences")
