@@ -83,34 +83,39 @@ def dequant_bytes(w: wl.Workload, n_pages: int, n_pools: int) -> int:
 
 def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
     """Time the float64 oracle (as it stands) on a bounded sample of the same
-    workload: whole sequences of one layer, as many as fit ~budget_s."""
+    workload: one layer of the whole batch, run repeatedly for ~budget_s."""
     import oracle
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     from oracle_fixtures import make_paged  # test infrastructure (value draws + encode)
-    ctx_full = wl.context_lens(w)
-    n_seq = 1
-    sample_ctx = ctx_full.copy()
-    # one layer of the workload, restricted to its first sequences
-    kv = make_paged(w, value_seqs=list(range(min(4, w.batch))), with_bf16_pool=False)
-    spent, elapsed, done_tokens = 0, 0.0, 0
-    while elapsed < budget_s and n_seq <= min(4, w.batch):
-        sel = np.arange(n_seq)
-        t0 = time.perf_counter()
-        oracle.decode_attn(np.ascontiguousarray(kv.q[sel]), kv.k_mant, kv.k_exp, kv.v_mant,
-                           kv.v_exp, None, None, np.ascontiguousarray(kv.page_table[sel]),
-                           np.ascontiguousarray(kv.ctx[sel]), kv.num_kv_heads, kv.page_size,
-                           kv.scale)
+    kv = make_paged(w, with_bf16_pool=False)
+    reps, elapsed = 0, 0.0
+    t0 = time.perf_counter()
+    while elapsed < budget_s:
+        oracle.decode_attn(kv.q, kv.k_mant, kv.k_exp, kv.v_mant, kv.v_exp, None, None,
+                           kv.page_table, kv.ctx, kv.num_kv_heads, kv.page_size, kv.scale)
+        reps += 1
         elapsed = time.perf_counter() - t0
-        done_tokens = int(sample_ctx[sel].sum())
-        if elapsed * 2 > budget_s:
-            break
-        n_seq *= 2
-    nbytes = done_tokens * bfp8_bytes_per_token_layer(w.num_kv_heads, w.head_dim)
+    nbytes = reps * attn_bytes(w, kv.ctx)
     cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     return {"value": round(nbytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": cores,
             "kind": "oracle",
-            "sample": f"float64 oracle attention, 1 layer, {n_seq} of {w.batch} sequences "
-                      f"({done_tokens} tokens, all {w.num_q_heads} heads): {elapsed:.2f} s"}
+            "sample": f"float64 oracle attention over one layer of the full batch "
+                      f"({int(kv.ctx.sum())} tokens, {w.num_q_heads} heads), {reps} runs "
+                      f"in {elapsed:.1f} s; same byte accounting as the GPU figure"}
+
+
+def copy_probe(mib: int, reps: int = 5) -> None:
+    """Plain device copy of a known size, for scaling HBM byte counters."""
+    import torch
+    n = mib << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "reps": reps}))
 
 
 # --------------------------------------------------------------------- main
@@ -123,12 +128,18 @@ def main():
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--tokens-per-split", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--resident-layers", type=int, default=0,
                     help="layers kept resident (0 = all that the workload defines, 8 for the trace mix)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
+
+    if args.copy_probe_mib:
+        copy_probe(args.copy_probe_mib)
+        return
 
     import torch
     import paper_2606_29986_amd as hma

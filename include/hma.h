@@ -124,8 +124,9 @@ HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_e
  *   q          uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
  *   k_mant, v_mant  uint8 mantissa pools, 16-byte aligned
  *   k_exp, v_exp    uint8 exponent pools, 16-byte aligned
- *   k_bf16, v_bf16  uint16 BF16 pools, 16-byte aligned; may be NULL when no
- *              page-table entry carries HMA_PAGE_BF16
+ *   k_bf16, v_bf16  uint16 BF16 pools, 16-byte aligned; both NULL or both
+ *              set.  When NULL the HMA_PAGE_BF16 bit is ignored and every
+ *              page is read from the BFP8 pools.
  *   page_table int32 [batch][max_pages_per_seq]
  *   context_lens  int32 [batch], each in [0, max_context_len]
  *   max_context_len  host-side bound that sizes the launch (no device read
@@ -135,7 +136,7 @@ HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_e
  *   scale      softmax scale (typically 1/sqrt(128))
  *   tokens_per_split  0 = chosen by the library (see
  *              hma_decode_attn_tokens_per_split); else a positive multiple
- *              of 32
+ *              of 32, at most 16384
  *   out        uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
  *   lse        float32 [batch][num_q_heads], or NULL
  *   workspace  device buffer of at least hma_decode_attn_workspace_bytes()

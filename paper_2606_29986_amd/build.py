@@ -26,7 +26,7 @@ ARCH = "gfx950"
 def hipcc_command(out: str, extra=()) -> list:
     cmd = ["hipcc", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-fvisibility=hidden", "-Wall", "-Wno-unused-command-line-argument",
+           "-fvisibility=hidden", "-Wall", "-Wno-unused-command-line-argument", "-Wno-inline-asm",
            f"-I{INCLUDE}", f"-I{CSRC}", *extra, "-x", "hip"]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]
     cmd += ["-o", out]

@@ -15,9 +15,9 @@ constexpr int32_t kSupportedHeadDim = 128;
 constexpr int32_t kSupportedPageSize = 16;
 constexpr int32_t kMaxGroup = 16;            // query heads per KV head (MFMA N = 16)
 constexpr int32_t kSplitQuantum = 32;        // tokens per attention step
-constexpr int64_t kTargetWorkgroups = 2048;  // auto split: aim for ~8 workgroups per CU
-constexpr int32_t kMinAutoSplit = 512;
-constexpr int32_t kMaxAutoSplit = 1024;
+constexpr int64_t kTargetWorkgroups = 512;   // auto split: two resident workgroups per CU
+constexpr int32_t kMinAutoSplit = 256;
+constexpr int32_t kMaxAutoSplit = 2048;
 
 bool aligned(const void *p, uintptr_t a)
 {
@@ -39,7 +39,7 @@ int32_t auto_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx)
     const int64_t pairs = (int64_t)batch * hkv;
     const int32_t whole = round_up(max_ctx > 0 ? max_ctx : 1, kSplitQuantum);
     int64_t tps = (pairs * (int64_t)max_ctx + kTargetWorkgroups - 1) / kTargetWorkgroups;
-    tps = round_up(tps, 256);
+    tps = round_up(tps, kSplitQuantum);
     if (tps < kMinAutoSplit)
         tps = kMinAutoSplit;
     if (tps > kMaxAutoSplit)
@@ -122,7 +122,8 @@ size_t hma_decode_attn_workspace_bytes(int32_t batch, int32_t num_q_heads, int32
 {
     if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
         return (size_t)-1;
-    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0)
+    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0 ||
+        tokens_per_split > hma::kMaxTokensPerSplit)
         return (size_t)-1;
     const int32_t tps = tokens_per_split ? tokens_per_split
                                          : auto_tokens_per_split(batch, num_kv_heads, max_context_len);
@@ -144,7 +145,8 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
         return HMA_EUNSUPPORTED;
     if (num_q_heads / num_kv_heads > kMaxGroup)
         return HMA_EUNSUPPORTED;
-    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0)
+    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0 ||
+        tokens_per_split > hma::kMaxTokensPerSplit)
         return HMA_EINVAL;
     if (max_pages_per_seq < 0 || (int64_t)max_context_len > (int64_t)max_pages_per_seq * page_size)
         return HMA_EINVAL;

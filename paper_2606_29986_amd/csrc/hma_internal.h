@@ -7,6 +7,11 @@
 
 namespace hma {
 
+// Longest split the attention kernel accepts: its page-table slice is staged
+// in LDS (4 bytes per 16-token page).
+constexpr int32_t kMaxTokensPerSplit = 16384;
+constexpr int kMaxSplitPages = kMaxTokensPerSplit / 16;
+
 // Returns 0 on a successful launch, -1 if the launch failed.
 int launch_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst,
                               const int32_t *src_pages, const int32_t *dst_pages,
