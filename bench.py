@@ -15,7 +15,10 @@ Prints ONE JSON line.  value = effective KV GB/s of the step: the bytes the
 method must move (BFP8 pages at 1.0625 B/element, BF16 pages at 2 B/element,
 plus Q, output and page table; for the rebuild, BFP8 read + BF16 written)
 divided by the step time.  Per-kernel figures come from HIP events recorded
-on the launch stream around every launch.
+on the launch stream: the attention launches of a step run back to back
+between one event pair (average launch duration, dispatch gaps included);
+attn_us_p50/p99 come from a separate untimed pass with an event pair around
+each launch.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload 3]
 """
@@ -232,57 +235,69 @@ def main():
     n_launch = w.layers
     events = []
 
-    def step(record):
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    def step(record, per_launch=False):
+        """One pass of the path.  Uniform workloads: the attention launches of
+        all layers run back to back and are bracketed by one event pair (their
+        average is the per-launch duration, dispatch gaps included), then the
+        rebuild launch has its own pair.  With per_launch (a separate,
+        untimed pass) every attention launch gets its own pair, for the
+        latency distribution.  Mixed workload: attention and rebuild alternate
+        per layer, each launch bracketed."""
         evs = []
-        for layer in range(n_launch):
-            slot = layer % resident
-            if record:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-            attn_launch(slot)
-            if record:
-                e1 = torch.cuda.Event(enable_timing=True)
-                e1.record(stream)
-            if mixed:
+        if mixed:
+            for layer in range(n_launch):
+                slot = layer % resident
+                e0 = ev() if record else None
+                attn_launch(slot)
+                e1 = ev() if record else None
                 dequant_launch(slot)
                 if record:
-                    e2 = torch.cuda.Event(enable_timing=True)
-                    e2.record(stream)
-                    evs.append((e0, e1, e2))
-            elif record:
-                evs.append((e0, e1, None))
-        if not mixed:
-            if record:
-                d0 = torch.cuda.Event(enable_timing=True)
-                d0.record(stream)
+                    evs.append(("attn", e0, e1, 1))
+                    evs.append(("dq", e1, ev(), 1))
+        else:
+            if record and not per_launch:
+                e0 = ev()
+            for layer in range(n_launch):
+                if per_launch:
+                    a0 = ev()
+                attn_launch(layer % resident)
+                if per_launch:
+                    evs.append(("attn", a0, ev(), 1))
+            if record and not per_launch:
+                e1 = ev()
+                evs.append(("attn", e0, e1, n_launch))
             dequant_launch()
-            if record:
-                d1 = torch.cuda.Event(enable_timing=True)
-                d1.record(stream)
-                evs.append((d0, None, d1))
-        if record:
-            events.append(evs)
+            if record and not per_launch:
+                evs.append(("dq", e1, ev(), 1))
+        return evs
 
     for _ in range(args.warmup):
         step(False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step(True)
+        events.append(step(True))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
     attn_us, dq_us = [], []
     for evs in events:
-        for e0, e1, e2 in evs:
-            if e1 is not None:
-                attn_us.append(e0.elapsed_time(e1) * 1e3)
-                if e2 is not None:
-                    dq_us.append(e1.elapsed_time(e2) * 1e3)
-            else:
-                dq_us.append(e0.elapsed_time(e2) * 1e3)
+        for kind, e0, e1, n in evs:
+            (attn_us if kind == "attn" else dq_us).append(e0.elapsed_time(e1) * 1e3 / n)
     attn_us = np.array(attn_us)
     dq_us = np.array(dq_us)
+    # latency distribution over single launches (outside the timed region)
+    if mixed:
+        single = attn_us
+    else:
+        evs = step(True, per_launch=True)
+        torch.cuda.synchronize()
+        single = np.array([e0.elapsed_time(e1) * 1e3 for _, e0, e1, _ in evs])
 
     a_bytes = attn_bytes(w, ctx, bf16_tokens)
     if mixed:
@@ -331,8 +346,8 @@ def main():
                      "%d layers (%d pages each)" % (n_launch, w.layers, dq_pages)),
         },
         "attn_us_per_layer": round(attn_mean, 3),
-        "attn_us_p50": round(float(np.percentile(attn_us, 50)), 3),
-        "attn_us_p99": round(float(np.percentile(attn_us, 99)), 3),
+        "attn_us_p50": round(float(np.percentile(single, 50)), 3),
+        "attn_us_p99": round(float(np.percentile(single, 99)), 3),
         "attn_GBps": round(attn_gbps, 2),
         "attn_frac_hbm_peak": round(attn_gbps / HBM_PEAK_GBPS, 4),
         "dequant_us": round(float(dq_us.mean()), 3),

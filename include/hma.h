@@ -136,7 +136,7 @@ HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_e
  *   scale      softmax scale (typically 1/sqrt(128))
  *   tokens_per_split  0 = chosen by the library (see
  *              hma_decode_attn_tokens_per_split); else a positive multiple
- *              of 32, at most 16384
+ *              of page_size (16), at most 16384
  *   out        uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
  *   lse        float32 [batch][num_q_heads], or NULL
  *   workspace  device buffer of at least hma_decode_attn_workspace_bytes()
@@ -157,7 +157,7 @@ HMA_API int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const
 
 /*
  * Split length the library uses for tokens_per_split = 0 (host only, no HIP
- * call).  Returns a positive multiple of 32, or 0 on invalid sizes.
+ * call).  Returns a positive multiple of 16, or 0 on invalid sizes.
  */
 HMA_API int32_t hma_decode_attn_tokens_per_split(int32_t batch, int32_t num_q_heads,
                                          int32_t num_kv_heads, int32_t max_context_len);

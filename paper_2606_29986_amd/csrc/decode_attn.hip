@@ -644,38 +644,62 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void decode_attn_bfp8_kernel(At
         return;
 
     if (head_ok) {
-        // online log-sum-exp fold of every split's partial, in split order (the
-        // result must not depend on which workgroup arrived last)
+        // log-sum-exp merge of every split's partial: the maximum over the
+        // splits first, then the weighted sums in split order (the result
+        // must not depend on which workgroup arrived last).  Loads are issued
+        // a batch ahead of their use, so the merge pays about one
+        // device-coherent load latency per pass instead of one per split.
+        constexpr int kMlBatch = 8;
         M = -INFINITY;
+        for (int t0 = 0; t0 < n_split_b; t0 += kMlBatch) {
+            float mt[kMlBatch];
+#pragma unroll
+            for (int u = 0; u < kMlBatch; u++) {
+                const int t = min(t0 + u, n_split_b - 1);
+                mt[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    rs_ml, (uint32_t)((t * p.g + r) * 8), 0, kCoherent));
+            }
+#pragma unroll
+            for (int u = 0; u < kMlBatch; u++)
+                M = fmaxf(M, mt[u]);     // clamped repeats of the last split change nothing
+        }
         L = 0.0f;
 #pragma unroll
         for (int n = 0; n < 8; n++)
             O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int t = 0; t < n_split_b; t++) {
-            const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(rs_ml, (uint32_t)((t * p.g + r) * 8), 0,
-                                                                   kCoherent);
+        f32x4_t cur[8];
+        u32x2_t cur_ml;
+        auto load_split = [&](int t, f32x4_t(&dst)[8], u32x2_t &ml) {
             const uint32_t ob = (uint32_t)(((t * p.g + r) * kHeadDim + 32 * G) * 4);
-            f32x4_t lo4[4], hi4[4];
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                lo4[i] = __builtin_bit_cast(
+                dst[i] = __builtin_bit_cast(
                     f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, ob + 32 * i, 0, kCoherent));
-                hi4[i] = __builtin_bit_cast(
+                dst[4 + i] = __builtin_bit_cast(
                     f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, ob + 32 * i + 16, 0, kCoherent));
             }
-            const float mt = __uint_as_float(v.x);
-            const float Mn = fmaxf(M, mt);
-            const float a = __builtin_amdgcn_exp2f(M - Mn);     // 0 for the first split
-            const float c = __builtin_amdgcn_exp2f(mt - Mn);
-            L = fmaf(L, a, __uint_as_float(v.y) * c);
-            M = Mn;
+            ml = __builtin_amdgcn_raw_buffer_load_b64(rs_ml, (uint32_t)((t * p.g + r) * 8), 0, kCoherent);
+        };
+        load_split(0, cur, cur_ml);
+        for (int t = 0; t < n_split_b; t++) {
+            // the next split's loads go out before this one is folded (past
+            // the end the last split is re-read and not used)
+            f32x4_t nxt[8];
+            u32x2_t nxt_ml;
+            load_split(min(t + 1, n_split_b - 1), nxt, nxt_ml);
+            const float c = __builtin_amdgcn_exp2f(__uint_as_float(cur_ml.x) - M);
+            L = fmaf(__uint_as_float(cur_ml.y), c, L);
 #pragma unroll
             for (int i = 0; i < 4; i++)
 #pragma unroll
                 for (int n = 0; n < 4; n++) {
-                    O[n][i] = fmaf(O[n][i], a, lo4[i][n] * c);
-                    O[4 + n][i] = fmaf(O[4 + n][i], a, hi4[i][n] * c);
+                    O[n][i] = fmaf(cur[i][n], c, O[n][i]);
+                    O[4 + n][i] = fmaf(cur[4 + i][n], c, O[4 + n][i]);
                 }
+#pragma unroll
+            for (int k = 0; k < 8; k++)
+                cur[k] = nxt[k];
+            cur_ml = nxt_ml;
         }
         store_out_row(p.out + out_row * kHeadDim + 32 * G, O, 1.0f / L);
         if (p.lse && G == 0)

@@ -14,7 +14,8 @@ namespace {
 constexpr int32_t kSupportedHeadDim = 128;
 constexpr int32_t kSupportedPageSize = 16;
 constexpr int32_t kMaxGroup = 16;            // query heads per KV head (MFMA N = 16)
-constexpr int32_t kSplitQuantum = 32;        // tokens per attention step
+constexpr int32_t kSplitQuantum = 16;        // splits hold whole pages
+constexpr int32_t kAutoSplitQuantum = 32;
 constexpr int64_t kTargetWorkgroups = 512;   // auto split: two resident workgroups per CU
 constexpr int32_t kMinAutoSplit = 256;
 constexpr int32_t kMaxAutoSplit = 2048;
@@ -39,7 +40,7 @@ int32_t auto_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx)
     const int64_t pairs = (int64_t)batch * hkv;
     const int32_t whole = round_up(max_ctx > 0 ? max_ctx : 1, kSplitQuantum);
     int64_t tps = (pairs * (int64_t)max_ctx + kTargetWorkgroups - 1) / kTargetWorkgroups;
-    tps = round_up(tps, kSplitQuantum);
+    tps = round_up(tps, kAutoSplitQuantum);
     if (tps < kMinAutoSplit)
         tps = kMinAutoSplit;
     if (tps > kMaxAutoSplit)

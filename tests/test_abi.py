@@ -49,7 +49,7 @@ def test_status_strings():
 
 def test_split_and_workspace_queries():
     tps = hma.tokens_per_split(16, 64, 8, 8192)
-    assert tps > 0 and tps % 32 == 0
+    assert tps > 0 and tps % 16 == 0
     S = -(-8192 // tps)
     ws = hma.workspace_bytes(16, 64, 8, 8192)
     pairs, g = 16 * 8, 8
@@ -59,9 +59,10 @@ def test_split_and_workspace_queries():
     # one split: no workspace
     assert hma.workspace_bytes(4, 32, 8, 512, 512) == 0
     assert hma.workspace_bytes(4, 32, 8, 0) == 0
-    # explicit split sizes must be multiples of 32
+    # explicit split sizes must be whole pages
+    assert hma.workspace_bytes(4, 32, 8, 512, 48) > 0
     with pytest.raises(hma.HmaError):
-        hma.workspace_bytes(4, 32, 8, 512, 48)
+        hma.workspace_bytes(4, 32, 8, 512, 40)
     with pytest.raises(hma.HmaError):
         hma.workspace_bytes(4, 30, 8, 512)
     assert hma.tokens_per_split(4, 30, 8, 512) == 0
@@ -115,7 +116,7 @@ def test_attn_validation():
     assert _attn(Hq=8 * 17) == hma.HMA_EUNSUPPORTED        # group of 17
     assert _attn(D=64) == hma.HMA_EUNSUPPORTED
     assert _attn(P=32) == hma.HMA_EUNSUPPORTED
-    assert _attn(tps=48) == hma.HMA_EINVAL
+    assert _attn(tps=40) == hma.HMA_EINVAL                 # not whole pages
     assert _attn(tps=-32) == hma.HMA_EINVAL
     assert _attn(maxctx=-1) == hma.HMA_EINVAL
     assert _attn(maxp=100) == hma.HMA_EINVAL               # 8192 tokens need 512 pages
