@@ -8,10 +8,12 @@
 // Work decomposition.  One workgroup (4 waves) owns one (sequence b, KV head
 // j, split s): the tokens [s*tps, min(ctx_b, (s+1)*tps)).  The split's slice
 // of the page table is staged in LDS once.  A wave walks the split one
-// 16-token page at a time, page c going to wave c % 4.  For pure-BFP8 page
-// tables each page's four tiles are copied into LDS by direct-to-LDS loads,
-// the next page's loads in flight while the current page is decoded and
-// multiplied; when BF16 pages may appear, pages are loaded into registers.
+// 16-token page at a time, page c going to wave c % 4.  A page's bytes are
+// loaded straight into registers in the lane layout of the matrix-core
+// operands (no LDS round trip: for this scattered-page access pattern plain
+// vector loads sustain a higher HBM rate than direct-to-LDS copies), and the
+// loads of the wave's next page are in flight while the current page is
+// decoded and multiplied.
 //
 // Per page, with g = Hq/Hkv query heads padded to 16:
 //   QK : S[16 tok][16 heads] = K_page[16 tok][128] . Q^T[128][16]
@@ -186,83 +188,22 @@ __device__ __forceinline__ void load_page_regs(PageRaw<true> &c, const PageInfo 
     }
 }
 
-// ----------------------------------------------- LDS staging (BFP8 pages)
-//
-// A staging buffer holds one page (4352 bytes):
-//   [0, 2048)     K mantissa tile, 16-byte units XOR-swizzled: unit 8*row + u
-//                 holds bytes [16*(u ^ (row & 7)), +16) of token row `row`, so
-//                 the lanes' 128-bit operand reads hit distinct banks
-//   [2048, 2176)  K exponent tile [token][8]
-//   [2176, 4224)  V mantissa tile [token][128]
-//   [4224, 4352)  V exponent tile [token][8]
-// It is filled with direct-to-LDS loads (global_load_lds_dwordx4): each of
-// the 6 load instructions of a page moves a contiguous 1 KB (or 128 B) of one
-// tile, and no VGPR holds data in flight.
-constexpr int kPageBytes = 2 * (kTileMant + kTileExp);
-constexpr int kDmaPerPage = 6;
-
-// Wait until at most N vector-memory instructions of this wave are in flight
-// (they retire in order); also a compiler memory barrier.
-template <int N>
-__device__ __forceinline__ void wait_vmem()
-{
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// One direct-to-LDS load: every active lane copies 16 bytes from `src` to LDS
-// address lds + 16 * lane.  Written as assembly so that the compiler does not
-// track it as an LDS write (it would otherwise drain every such load before
-// any LDS read): the explicit wait_vmem calls order it against the reads of
-// the buffer it fills.  M0 is named as clobbered; nothing else in these
-// kernels keeps a value in M0 (LDS instructions on gfx9+ do not use it).
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void *src, uint32_t lds)
-{
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-                 :: "v"(src), "s"(lds) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-__device__ __forceinline__ uint32_t lds_addr(const void *ptr)
-{
-    typedef const __attribute__((address_space(3))) uint8_t *lds_ptr_t;
-    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_ptr_t)ptr);
-}
-
-__device__ __forceinline__ void dma_page(uint32_t dst, const AttnParams &p, const PageInfo &inf, int j,
-                                         int lane)
+// Register loads of one BFP8 page (the pure-BFP8 path), in the lane layout
+// of the matrix-core operands: 11 loads per wave and page.
+__device__ __forceinline__ void load_page_regs(PageRaw<false> &c, const PageInfo &inf, const AttnParams &p,
+                                               int j, int G, int r)
 {
     const int64_t tile = (int64_t)(inf.ent & kIdMask) * p.hkv + j;
-    const uint8_t *km = p.k_mant + tile * kTileMant;
-    const uint8_t *vm = p.v_mant + tile * kTileMant;
-#pragma unroll
-    for (int h = 0; h < 2; h++) {
-        const int row = 8 * h + (lane >> 3);
-        const int unit = (lane & 7) ^ (row & 7);
-        dma16(km + row * kHeadDim + 16 * unit, dst + 1024 * h);
-    }
-#pragma unroll
-    for (int h = 0; h < 2; h++)
-        dma16(vm + 1024 * h + 16 * lane, dst + kTileMant + kTileExp + 1024 * h);
-    if (lane < 8) {
-        dma16(p.k_exp + tile * kTileExp + 16 * lane, dst + kTileMant);
-        dma16(p.v_exp + tile * kTileExp + 16 * lane, dst + 2 * kTileMant + kTileExp);
-    }
-}
-
-// The lane's operand bytes of a staged page.
-__device__ __forceinline__ void lds_read_page(const uint8_t *b, PageRaw<false> &c, int G, int r)
-{
-    c.km0 = *reinterpret_cast<const u32x4_t *>(b + 16 * (8 * r + (G ^ (r & 7))));
-    c.km1 = *reinterpret_cast<const u32x4_t *>(b + 16 * (8 * r + ((4 + G) ^ (r & 7))));
-    c.ke = *reinterpret_cast<const u32x2_t *>(b + kTileMant + kExpPerRow * r);
-    const uint8_t *v = b + kTileMant + kTileExp;
-    const uint8_t *ve = v + kTileMant;
+    const uint8_t *kt = p.k_mant + tile * kTileMant;
+    const uint8_t *vt = p.v_mant + tile * kTileMant;
+    const uint8_t *vx = p.v_exp + tile * kTileExp;
+    c.km0 = *reinterpret_cast<const u32x4_t *>(kt + r * kHeadDim + 16 * G);
+    c.km1 = *reinterpret_cast<const u32x4_t *>(kt + r * kHeadDim + 64 + 16 * G);
+    c.ke = *reinterpret_cast<const u32x2_t *>(p.k_exp + tile * kTileExp + r * kExpPerRow);
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        c.vm[i] = *reinterpret_cast<const u32x2_t *>(v + (4 * G + i) * kHeadDim + 8 * r);
-        c.ve[i] = ve[(4 * G + i) * kExpPerRow + (r >> 1)];
+        c.vm[i] = *reinterpret_cast<const u32x2_t *>(vt + (4 * G + i) * kHeadDim + 8 * r);
+        c.ve[i] = vx[(4 * G + i) * kExpPerRow + (r >> 1)];
     }
 }
 
@@ -295,6 +236,57 @@ __device__ __forceinline__ void v_pairs_bfp8(u32x2_t va, uint32_t ea, u32x2_t vb
         for (int n4 = 0; n4 < 4; n4++)
             pr[4 * d + n4] = pack_bf16_signed(bfp8_mag_f32(ma, n4, esa), bfp8_mag_f32(mb, n4, esb),
                                               wa, n4, wb, n4);
+    }
+}
+
+// Block exponents of one BFP8 page as one lane uses them, as 133 - E in
+// 16-bit halves: k = {block G, block 4 + G} of token r; v01, v23 = {token 4G,
+// 4G + 1} and {4G + 2, 4G + 3} of channel block r / 2.
+struct ExpHalves {
+    uint32_t k, v01, v23;
+};
+
+__device__ __forceinline__ ExpHalves exp_halves(u32x2_t ke, uint32_t e0, uint32_t e1, uint32_t e2,
+                                                uint32_t e3, int G)
+{
+    const uint32_t bias = 0x00850085u;     // 133 in each half
+    ExpHalves h;
+    h.k = pk_sub_u16(bias, __builtin_amdgcn_perm(ke.y, ke.x, 0x0C000C00u | ((uint32_t)(4 + G) << 16) | (uint32_t)G));
+    h.v01 = pk_sub_u16(bias, __builtin_amdgcn_perm(e1, e0, 0x0C040C00u));
+    h.v23 = pk_sub_u16(bias, __builtin_amdgcn_perm(e3, e2, 0x0C040C00u));
+    return h;
+}
+
+// True (for the whole wave) when every block of the page has 7 <= E <= 133,
+// i.e. 133 - E <= 126 as an unsigned 16-bit value, so the packed route is exact.
+__device__ __forceinline__ bool fast_route(const ExpHalves &h)
+{
+    const uint32_t mx = pk_max_u16(pk_max_u16(h.k, h.v01), h.v23);
+    const bool out_of_range = (pk_add_sat_u16(mx, 0x7F817F81u) & 0x80008000u) != 0;   // a half >= 127
+    return __builtin_amdgcn_ballot_w64(out_of_range) == 0;
+}
+
+// K operands on the packed route.
+__device__ __forceinline__ void k_operands_fast(u32x4_t km0, u32x4_t km1, uint32_t hk, u32x4_t (&A)[4])
+{
+    const uint32_t d = pk_shl7_u16(hk);
+    bfp8_block_to_bf16_fast(km0, __builtin_amdgcn_perm(d, d, 0x01000100u), A[0], A[1]);
+    bfp8_block_to_bf16_fast(km1, __builtin_amdgcn_perm(d, d, 0x03020302u), A[2], A[3]);
+}
+
+// V^T operand pairs on the packed route (hab: slot a in the low half, b high).
+__device__ __forceinline__ void v_pairs_fast(u32x2_t va, u32x2_t vb, uint32_t hab, uint32_t (&pr)[8])
+{
+    const uint32_t d = pk_shl7_u16(hab);
+#pragma unroll
+    for (int dd = 0; dd < 2; dd++) {
+        const uint32_t wa = dd ? va.y : va.x;
+        const uint32_t wb = dd ? vb.y : vb.x;
+        const uint32_t ma = magnitudes(wa);
+        const uint32_t mb = magnitudes(wb);
+#pragma unroll
+        for (int n4 = 0; n4 < 4; n4++)
+            pr[4 * dd + n4] = pack_bf16_scaled_signed(mag_byte(ma, n4), mag_byte(mb, n4), d, wa, n4, wb, n4);
     }
 }
 
@@ -334,6 +326,19 @@ __device__ __forceinline__ void process_page(const PageRaw<MIXED> &c, const Page
                                              const u32x4_t (&qB)[4], float scale_log2, int G,
                                              SoftmaxState &st, f32x4_t (&O)[8])
 {
+    // ---- decode route of a BFP8 page (uniform over the wave)
+    ExpHalves eh;
+    bool fast = false;
+    if constexpr (MIXED) {
+        if (!(inf.ent & kTagBf16)) {
+            eh = exp_halves(u32x2_t{c.k[2].x, c.k[2].y}, c.v[0].z, c.v[1].z, c.v[2].z, c.v[3].z, G);
+            fast = fast_route(eh);
+        }
+    } else {
+        eh = exp_halves(c.ke, c.ve[0], c.ve[1], c.ve[2], c.ve[3], G);
+        fast = fast_route(eh);
+    }
+
     // ---- QK^T
     u32x4_t A[4];
     if constexpr (MIXED) {
@@ -341,11 +346,16 @@ __device__ __forceinline__ void process_page(const PageRaw<MIXED> &c, const Page
 #pragma unroll
             for (int kk = 0; kk < 4; kk++)
                 A[kk] = c.k[kk];
+        } else if (fast) {
+            k_operands_fast(c.k[0], c.k[1], eh.k, A);
         } else {
             k_operands_bfp8(c.k[0], c.k[1], u32x2_t{c.k[2].x, c.k[2].y}, G, A);
         }
     } else {
-        k_operands_bfp8(c.km0, c.km1, c.ke, G, A);
+        if (fast)
+            k_operands_fast(c.km0, c.km1, eh.k, A);
+        else
+            k_operands_bfp8(c.km0, c.km1, c.ke, G, A);
     }
     f32x4_t S = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -357,15 +367,21 @@ __device__ __forceinline__ void process_page(const PageRaw<MIXED> &c, const Page
 #pragma unroll
     for (int k2 = 0; k2 < 2; k2++) {
         uint32_t pr[8];
+        const uint32_t hab = k2 ? eh.v23 : eh.v01;
         if constexpr (MIXED) {
             const u32x4_t va = c.v[2 * k2];
             const u32x4_t vb = c.v[2 * k2 + 1];
             if (inf.ent & kTagBf16)
                 v_pairs_bf16(va, vb, pr);
+            else if (fast)
+                v_pairs_fast(u32x2_t{va.x, va.y}, u32x2_t{vb.x, vb.y}, hab, pr);
             else
                 v_pairs_bfp8(u32x2_t{va.x, va.y}, va.z, u32x2_t{vb.x, vb.y}, vb.z, pr);
         } else {
-            v_pairs_bfp8(c.vm[2 * k2], c.ve[2 * k2], c.vm[2 * k2 + 1], c.ve[2 * k2 + 1], pr);
+            if (fast)
+                v_pairs_fast(c.vm[2 * k2], c.vm[2 * k2 + 1], hab, pr);
+            else
+                v_pairs_bfp8(c.vm[2 * k2], c.ve[2 * k2], c.vm[2 * k2 + 1], c.ve[2 * k2 + 1], pr);
         }
 #pragma unroll
         for (int n = 0; n < 8; n++) {
@@ -443,8 +459,7 @@ __device__ __forceinline__ void process_page(const PageRaw<MIXED> &c, const Page
 // ------------------------------------------------------------------ kernel
 
 constexpr int kMergeBytes = ((kAttnWaves - 1) * 32 * 64 + 2 * kAttnWaves * 16) * 4;
-constexpr int kStageBytes = 2 * kAttnWaves * kPageBytes;
-static_assert(kMergeBytes <= kStageBytes, "wave merge must fit in the staging buffers");
+constexpr int kStages = 2;   // pages of one wave in registers: kStages - 1 in flight + 1 computed
 
 template <bool MIXED>
 __global__ __launch_bounds__(64 * kAttnWaves, 2) void decode_attn_bfp8_kernel(AttnParams p)
@@ -481,8 +496,8 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void decode_attn_bfp8_kernel(At
     const int n_split_b = (ctx + p.tps - 1) / p.tps;
     const int n_pages = (n_tok + kPageSize - 1) / kPageSize;
 
-    // LDS: page staging buffers [2][wave] (pure-BFP8 path), reused for the wave merge
-    __shared__ __attribute__((aligned(16))) uint8_t sm_buf[MIXED ? kMergeBytes : kStageBytes];
+    // LDS: the wave merge, and this split's slice of the page table
+    __shared__ __attribute__((aligned(16))) uint8_t sm_buf[kMergeBytes];
     __shared__ uint32_t sm_pt[kMaxSplitPages];
 
     // stage this split's page-table slice in LDS
@@ -510,52 +525,36 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void decode_attn_bfp8_kernel(At
     for (int n = 0; n < 8; n++)
         O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    if constexpr (MIXED) {
-        // mixed page formats: register loads, one page at a time
-        for (int pi = wave; pi < n_pages; pi += kAttnWaves) {
-            PageRaw<true> rc;
-            const PageInfo ic = page_info(sm_pt, pi, n_tok);
-            load_page_regs(rc, ic, p, j, G, r);
-            process_page<true>(rc, ic, qB, p.scale_log2, G, st, O);
+    // Register pipeline: the loads of the wave's next kStages - 1 pages are in
+    // flight while the current page is decoded and multiplied (page k of the
+    // wave lives in register set k % kStages).  Past the wave's last page the
+    // prefetch re-requests that page (a cache hit), so the loop has no branch
+    // between a load and its use.
+    const int my_pages = n_pages > wave ? (n_pages - wave + kAttnWaves - 1) / kAttnWaves : 0;
+    if (my_pages > 0) {
+        auto page_at = [&](int k) {
+            return page_info(sm_pt, wave + min(k, my_pages - 1) * kAttnWaves, n_tok);
+        };
+        PageRaw<MIXED> c[kStages];
+        PageInfo ci[kStages];
+#pragma unroll
+        for (int q = 0; q + 1 < kStages; q++) {
+            ci[q] = page_at(q);
+            load_page_regs(c[q], ci[q], p, j, G, r);
         }
-    } else {
-        // staged pipeline: page k of this wave lives in buffer k % 2; the next
-        // page's direct-to-LDS loads are issued before the current page is read
-        // and computed.  The prefetch is issued unconditionally (past the last
-        // page it re-requests the current page into the idle buffer, served by
-        // the cache), so no branch separates a load from its wait and the wait
-        // before each read covers exactly the page being read.
-        const int my_pages = n_pages > wave ? (n_pages - wave + kAttnWaves - 1) / kAttnWaves : 0;
-        if (my_pages > 0) {
-            const uint8_t *buf0 = sm_buf + wave * kPageBytes;
-            const uint8_t *buf1 = sm_buf + (kAttnWaves + wave) * kPageBytes;
-            const uint32_t lds0 = lds_addr(buf0), lds1 = lds_addr(buf1);
-            PageInfo c0 = page_info(sm_pt, wave, n_tok), c1;
-            dma_page(lds0, p, c0, j, lane);
-            for (int k = 0; k < my_pages; k += 2) {
-                c1 = k + 1 < my_pages ? page_info(sm_pt, wave + (k + 1) * kAttnWaves, n_tok) : c0;
-                dma_page(lds1, p, c1, j, lane);
-                wait_vmem<kDmaPerPage>();
-                {
-                    PageRaw<false> rc;
-                    lds_read_page(buf0, rc, G, r);
-                    process_page<false>(rc, c0, qB, p.scale_log2, G, st, O);
-                }
-                if (k + 1 >= my_pages)
-                    break;
-                c0 = k + 2 < my_pages ? page_info(sm_pt, wave + (k + 2) * kAttnWaves, n_tok) : c1;
-                dma_page(lds0, p, c0, j, lane);
-                wait_vmem<kDmaPerPage>();
-                {
-                    PageRaw<false> rc;
-                    lds_read_page(buf1, rc, G, r);
-                    process_page<false>(rc, c1, qB, p.scale_log2, G, st, O);
-                }
+        for (int k = 0; k < my_pages; k += kStages) {
+#pragma unroll
+            for (int q = 0; q < kStages; q++) {
+                const int qn = (q + kStages - 1) % kStages;     // set freed by the previous page
+                ci[qn] = page_at(k + q + kStages - 1);
+                load_page_regs(c[qn], ci[qn], p, j, G, r);
+                process_page<MIXED>(c[q], ci[q], qB, p.scale_log2, G, st, O);
+                if (k + q + 1 >= my_pages)
+                    break;      // leaves the outer loop too: k + kStages > my_pages
             }
-            wait_vmem<0>();     // the last prefetch has landed before the buffers are reused
         }
     }
-    // every wave is done with its staging buffers before they are reused
+    // every wave has its partial before the workgroup merge
     __syncthreads();
 
     // ---- merge the four waves of the workgroup through LDS
@@ -644,31 +643,14 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void decode_attn_bfp8_kernel(At
         return;
 
     if (head_ok) {
-        // log-sum-exp merge of every split's partial: the maximum over the
-        // splits first, then the weighted sums in split order (the result
-        // must not depend on which workgroup arrived last).  Loads are issued
-        // a batch ahead of their use, so the merge pays about one
-        // device-coherent load latency per pass instead of one per split.
-        constexpr int kMlBatch = 8;
+        // online log-sum-exp fold of every split's partial, in split order
+        // (the result must not depend on which workgroup arrived last); the
+        // next split's device-coherent loads are in flight while one is folded
         M = -INFINITY;
-        for (int t0 = 0; t0 < n_split_b; t0 += kMlBatch) {
-            float mt[kMlBatch];
-#pragma unroll
-            for (int u = 0; u < kMlBatch; u++) {
-                const int t = min(t0 + u, n_split_b - 1);
-                mt[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                    rs_ml, (uint32_t)((t * p.g + r) * 8), 0, kCoherent));
-            }
-#pragma unroll
-            for (int u = 0; u < kMlBatch; u++)
-                M = fmaxf(M, mt[u]);     // clamped repeats of the last split change nothing
-        }
         L = 0.0f;
 #pragma unroll
         for (int n = 0; n < 8; n++)
             O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        f32x4_t cur[8];
-        u32x2_t cur_ml;
         auto load_split = [&](int t, f32x4_t(&dst)[8], u32x2_t &ml) {
             const uint32_t ob = (uint32_t)(((t * p.g + r) * kHeadDim + 32 * G) * 4);
 #pragma unroll
@@ -680,26 +662,33 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void decode_attn_bfp8_kernel(At
             }
             ml = __builtin_amdgcn_raw_buffer_load_b64(rs_ml, (uint32_t)((t * p.g + r) * 8), 0, kCoherent);
         };
-        load_split(0, cur, cur_ml);
-        for (int t = 0; t < n_split_b; t++) {
-            // the next split's loads go out before this one is folded (past
-            // the end the last split is re-read and not used)
-            f32x4_t nxt[8];
-            u32x2_t nxt_ml;
-            load_split(min(t + 1, n_split_b - 1), nxt, nxt_ml);
-            const float c = __builtin_amdgcn_exp2f(__uint_as_float(cur_ml.x) - M);
-            L = fmaf(__uint_as_float(cur_ml.y), c, L);
+        auto fold = [&](const f32x4_t(&v)[8], u32x2_t ml) {
+            const float mt = __uint_as_float(ml.x);
+            const float Mn = fmaxf(M, mt);
+            const float a = __builtin_amdgcn_exp2f(M - Mn);     // 0 for the first split
+            const float c = __builtin_amdgcn_exp2f(mt - Mn);
+            L = fmaf(L, a, __uint_as_float(ml.y) * c);
+            M = Mn;
 #pragma unroll
             for (int i = 0; i < 4; i++)
 #pragma unroll
                 for (int n = 0; n < 4; n++) {
-                    O[n][i] = fmaf(cur[i][n], c, O[n][i]);
-                    O[4 + n][i] = fmaf(cur[4 + i][n], c, O[4 + n][i]);
+                    O[n][i] = fmaf(O[n][i], a, v[i][n] * c);
+                    O[4 + n][i] = fmaf(O[4 + n][i], a, v[4 + i][n] * c);
                 }
-#pragma unroll
-            for (int k = 0; k < 8; k++)
-                cur[k] = nxt[k];
-            cur_ml = nxt_ml;
+        };
+        // two register sets, alternating; past the end the last split is
+        // re-read and not used
+        f32x4_t va[8], vb[8];
+        u32x2_t ma, mb;
+        load_split(0, va, ma);
+        for (int t = 0; t < n_split_b; t += 2) {
+            load_split(min(t + 1, n_split_b - 1), vb, mb);
+            fold(va, ma);
+            if (t + 1 >= n_split_b)
+                break;
+            load_split(min(t + 2, n_split_b - 1), va, ma);
+            fold(vb, mb);
         }
         store_out_row(p.out + out_row * kHeadDim + 32 * G, O, 1.0f / L);
         if (p.lse && G == 0)

@@ -15,6 +15,13 @@
 //   5. a second v_perm_b32 moves the two sign bits to bits 15 and 31 and an
 //      AND-OR inserts them.
 // About 3.75 VALU operations per element.
+//
+// A faster route covers 7 <= E <= 133, where every nonzero element is a
+// normal BF16: the BF16 bits of the magnitude itself (exact, at most 7
+// significant bits) only need their exponent field lowered by 133 - E, which
+// one saturating 16-bit packed subtract does for two elements at once while
+// keeping zero at zero.  That replaces the two v_ldexp_f32 of a pair (about
+// 3.25 operations per element).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,6 +43,32 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint16_t u16x2_t __attribute__((ext_vector_type(2)));
+
+// Packed 16-bit integer helpers (v_pk_*_u16; integer ops, no packed FP32).
+__device__ __forceinline__ uint32_t pk_sub_u16(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2_t, a) - __builtin_bit_cast(u16x2_t, b));
+}
+__device__ __forceinline__ uint32_t pk_sub_sat_u16(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_sub_sat(__builtin_bit_cast(u16x2_t, a),
+                                                                      __builtin_bit_cast(u16x2_t, b)));
+}
+__device__ __forceinline__ uint32_t pk_add_sat_u16(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_add_sat(__builtin_bit_cast(u16x2_t, a),
+                                                                      __builtin_bit_cast(u16x2_t, b)));
+}
+__device__ __forceinline__ uint32_t pk_max_u16(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(u16x2_t, a),
+                                                                  __builtin_bit_cast(u16x2_t, b)));
+}
+__device__ __forceinline__ uint32_t pk_shl7_u16(uint32_t a)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2_t, a) << (uint16_t)7);
+}
 
 // byte-select constants for __builtin_amdgcn_perm(S0, S1, sel):
 // result byte i = byte sel_i of the 64-bit value {S0 (bytes 4..7), S1 (bytes 0..3)};
@@ -102,6 +135,41 @@ __device__ __forceinline__ void bfp8_block_to_bf16(u32x4_t w, int es, u32x4_t &l
     const u32x2_t d = bfp8_word_to_bf16(w.w, es);
     lo = u32x4_t{a.x, a.y, b.x, b.y};
     hi = u32x4_t{c.x, c.y, d.x, d.y};
+}
+
+// ---- fast route (7 <= E <= 133): `d` holds (133 - E) << 7 in each 16-bit
+// half, for the element that lands in that half.
+
+// Two exact magnitudes (lo, hi) -> BF16 pair scaled by 2^(E-133), with the
+// sign bits of byte ka of wa (-> bit 15) and byte kb of wb (-> bit 31).
+__device__ __forceinline__ uint32_t pack_bf16_scaled_signed(float lo, float hi, uint32_t d, uint32_t wa,
+                                                            int ka, uint32_t wb, int kb)
+{
+    uint32_t m = __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), kPermHiHalves);
+    m = pk_sub_sat_u16(m, d);
+    uint32_t s = __builtin_amdgcn_perm(wb, wa, sign_sel(ka, kb));
+    return (s & 0x80008000u) | m;
+}
+
+__device__ __forceinline__ u32x2_t bfp8_word_to_bf16_fast(uint32_t w, uint32_t d)
+{
+    const uint32_t mg = magnitudes(w);
+    const float f0 = mag_byte(mg, 0);
+    const float f1 = mag_byte(mg, 1);
+    const float f2 = mag_byte(mg, 2);
+    const float f3 = mag_byte(mg, 3);
+    return u32x2_t{pack_bf16_scaled_signed(f0, f1, d, w, 0, w, 1),
+                   pack_bf16_scaled_signed(f2, f3, d, w, 2, w, 3)};
+}
+
+__device__ __forceinline__ void bfp8_block_to_bf16_fast(u32x4_t w, uint32_t d, u32x4_t &lo, u32x4_t &hi)
+{
+    const u32x2_t a = bfp8_word_to_bf16_fast(w.x, d);
+    const u32x2_t b = bfp8_word_to_bf16_fast(w.y, d);
+    const u32x2_t c = bfp8_word_to_bf16_fast(w.z, d);
+    const u32x2_t e = bfp8_word_to_bf16_fast(w.w, d);
+    lo = u32x4_t{a.x, a.y, b.x, b.y};
+    hi = u32x4_t{c.x, c.y, e.x, e.y};
 }
 
 }  // namespace hma
