@@ -16,9 +16,11 @@ constexpr int32_t kSupportedPageSize = 16;
 constexpr int32_t kMaxGroup = 16;            // query heads per KV head (MFMA N = 16)
 constexpr int32_t kSplitQuantum = 16;        // splits hold whole pages
 constexpr int32_t kAutoSplitQuantum = 32;
-constexpr int64_t kTargetWorkgroups = 512;   // auto split: two resident workgroups per CU
+constexpr int64_t kComputeUnits = 256;       // MI355X
+constexpr int64_t kTargetWorkgroups = 2 * kComputeUnits;   // 4-wave workgroups: two per CU
 constexpr int32_t kMinAutoSplit = 256;
 constexpr int32_t kMaxAutoSplit = 2048;
+constexpr int32_t kMaxWideSplit = 8192;
 
 bool aligned(const void *p, uintptr_t a)
 {
@@ -35,10 +37,24 @@ bool attn_sizes_ok(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx)
     return batch >= 0 && hq > 0 && hkv > 0 && hq % hkv == 0 && max_ctx >= 0;
 }
 
+int32_t splits_for(int32_t max_ctx, int32_t tps);
+
+// Split length for tokens_per_split = 0.  When every (sequence, KV head) pair
+// fits in one pass of one workgroup per CU, the splits are sized for exactly
+// that (8-wave workgroups); otherwise they target two 4-wave workgroups per
+// CU.
 int32_t auto_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx)
 {
     const int64_t pairs = (int64_t)batch * hkv;
     const int32_t whole = round_up(max_ctx > 0 ? max_ctx : 1, kSplitQuantum);
+    int64_t wide = (pairs * (int64_t)max_ctx + kComputeUnits - 1) / kComputeUnits;
+    wide = round_up(wide, kAutoSplitQuantum);
+    if (wide < kMinAutoSplit)
+        wide = kMinAutoSplit;
+    if (wide > whole)
+        wide = whole;
+    if (wide <= kMaxWideSplit && pairs * splits_for(max_ctx, (int32_t)wide) <= kComputeUnits)
+        return (int32_t)wide;
     int64_t tps = (pairs * (int64_t)max_ctx + kTargetWorkgroups - 1) / kTargetWorkgroups;
     tps = round_up(tps, kAutoSplitQuantum);
     if (tps < kMinAutoSplit)
@@ -48,6 +64,13 @@ int32_t auto_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx)
     if (tps > whole)
         tps = whole;
     return (int32_t)tps;
+}
+
+// Waves per workgroup for a grid of `blocks` workgroups: 8 (one workgroup per
+// CU) when the grid fits in one pass over the CUs, else 4.
+int32_t waves_for(int64_t blocks)
+{
+    return blocks <= kComputeUnits ? 8 : 4;
 }
 
 int32_t splits_for(int32_t max_ctx, int32_t tps)
@@ -193,6 +216,7 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
     a.hkv = num_kv_heads;
     a.tps = tps;
     a.n_splits = n_splits;
+    a.waves = waves_for((int64_t)batch * num_kv_heads * n_splits);
     a.scale = scale;
     return hma::launch_decode_attn(a, static_cast<hipStream_t>(stream)) == 0 ? HMA_OK : HMA_EHIP;
 }

@@ -28,6 +28,7 @@ struct AttnLaunch {
     float *lse;
     void *workspace;
     int32_t max_pages, batch, hq, hkv, tps, n_splits;
+    int32_t waves;          // 4 or 8 waves per workgroup
     float scale;
 };
 

@@ -26,86 +26,81 @@ from oracle_fixtures import PagedKV
 
 pytestmark = pytest.mark.gpu
 
-B, HKV, P, D = 64, 8, 16, 128
+HKV, P, D = 8, 16, 128
 SCALE = 1.0 / np.sqrt(128.0)
+# 32 sequences x 8 KV heads = 256 workgroups (one per CU: the 8-wave kernel);
+# 64 sequences = 512 workgroups (the 4-wave kernel)
+BATCHES = [32, 64]
 
 
-def _pages(rng):
-    """One page per sequence; ids permuted so placement is not the identity."""
+def _kv(rng, B, Hq, sweep, half):
+    """One page per sequence (ids permuted).  Token 0 of (sequence b, head j),
+    t = 8 b + j, gets bytes 128 * ((t // 256 + half) % 2) .. + 127 and every
+    block of that (page, head) tile of the swept stream gets exponent
+    min(t % 256, cap); the other stream has exponent 127 and random bytes."""
     ids = rng.permutation(B).astype(np.int32)
-    return ids, ids.reshape(B, 1)
-
-
-def _sweep_tile(mant, ex, ids, exps):
-    """Token 0 of (sequence b, head j) gets bytes 128*(t%2) .. +127 and every
-    block of that (page, head) tile gets exponent exps[t], t = 8 b + j."""
-    for b in range(B):
-        for j in range(HKV):
-            t = 8 * b + j
-            mant[ids[b], j, 0, :] = (128 * (t % 2) + np.arange(D)) % 256
-            ex[ids[b], j, :, :] = exps[t]
-
-
-def _kv(rng, Hq, sweep):
-    ids, pt = _pages(rng)
     k_mant = rng.integers(0, 256, (B, HKV, P, D), dtype=np.uint8)
     v_mant = rng.integers(0, 256, (B, HKV, P, D), dtype=np.uint8)
     k_exp = np.full((B, HKV, P, D // 16), 127, np.uint8)
     v_exp = np.full((B, HKV, P, D // 16), 127, np.uint8)
+    mant, ex, cap = (v_mant, v_exp, 254) if sweep == "v" else (k_mant, k_exp, 250)
     t = np.arange(B * HKV)
-    if sweep == "v":
-        exps = np.minimum(t // 2, 254)
-        _sweep_tile(v_mant, v_exp, ids, exps)
-    else:
-        exps = np.minimum(t // 2, 250)
-        _sweep_tile(k_mant, k_exp, ids, exps)
+    exps = np.minimum(t % 256, cap)
+    for b in range(B):
+        for j in range(HKV):
+            tt = 8 * b + j
+            mant[ids[b], j, 0, :] = (128 * ((tt // 256 + half) % 2) + np.arange(D)) % 256
+            ex[ids[b], j, :, :] = exps[tt]
     q = np.zeros((B, Hq, D), np.uint16)
     kv = PagedKV(q, k_mant, k_exp, v_mant, v_exp,
                  oracle.decode_blocks(k_mant, k_exp), oracle.decode_blocks(v_mant, v_exp),
-                 pt, np.ones(B, np.int32), HKV, P, SCALE)
+                 ids.reshape(B, 1), np.ones(B, np.int32), HKV, P, SCALE)
     return kv, ids, exps
 
 
+@pytest.mark.parametrize("B", BATCHES)
 @pytest.mark.parametrize("mixed_kernel", [False, True])
-def test_v_decode_exhaustive_through_single_token_output(mixed_kernel):
-    note(f"attn decode routes: V exhaustive, mixed-format kernel={mixed_kernel}")
-    rng = np.random.default_rng(11)
-    kv, ids, exps = _kv(rng, HKV, "v")
-    kv.q[:] = 0x3F80                          # q = 1.0: scores are finite and irrelevant
-    out, _ = DevKV(kv).attn(use_bf16_pools=mixed_kernel)
-    got = out.cpu().numpy().view(np.uint16).copy()
-    want = kv.v_bf16[ids, :, 0, :].copy()     # [B][Hkv][D] (g = 1: head j reads KV head j)
-    # a weighted sum that starts from +0 turns -0 into +0: compare zeros unsigned
-    got[got == 0x8000] = 0
-    want[want == 0x8000] = 0
-    bad = np.argwhere(got != want)
-    assert bad.size == 0, (f"{len(bad)} mismatches; first (b, h, c) {bad[:4].tolist()}, exponents "
-                           f"{[int(exps[8 * b + h]) for b, h, _ in bad[:4]]}")
+def test_v_decode_exhaustive_through_single_token_output(mixed_kernel, B):
+    for half in (0, 1):
+        note(f"attn decode routes: V exhaustive, B={B} half={half}, mixed-format kernel={mixed_kernel}")
+        rng = np.random.default_rng(11 + half)
+        kv, ids, exps = _kv(rng, B, HKV, "v", half)
+        kv.q[:] = 0x3F80                          # q = 1.0: scores are finite and irrelevant
+        out, _ = DevKV(kv).attn(use_bf16_pools=mixed_kernel)
+        got = out.cpu().numpy().view(np.uint16).copy()
+        want = kv.v_bf16[ids, :, 0, :].copy()     # [B][Hkv][D] (g = 1: head j reads KV head j)
+        # a weighted sum that starts from +0 turns -0 into +0: compare zeros unsigned
+        got[got == 0x8000] = 0
+        want[want == 0x8000] = 0
+        bad = np.argwhere(got != want)
+        assert bad.size == 0, (f"half {half}: {len(bad)} mismatches; first (b, h, c) {bad[:4].tolist()}, "
+                               f"exponents {[int(exps[8 * b + h]) for b, h, _ in bad[:4]]}")
 
 
+@pytest.mark.parametrize("B", BATCHES)
 @pytest.mark.parametrize("mixed_kernel", [False, True])
-def test_k_decode_exhaustive_through_single_token_lse(mixed_kernel):
-    note(f"attn decode routes: K exhaustive, mixed-format kernel={mixed_kernel}")
-    rng = np.random.default_rng(12)
+def test_k_decode_exhaustive_through_single_token_lse(mixed_kernel, B):
     g = 16
-    kv, ids, exps = _kv(rng, HKV * g, "k")
-    k_dec = oracle.bf16_to_f64(kv.k_bf16[ids, :, 0, :])      # [B][Hkv][D]
-    d = DevKV(kv)
-    for phase in range(8):
-        # head h of group j probes channel 8 (h % 16) + phase with weight 2^(126 - E)
-        q = np.zeros((B, HKV * g, D), np.uint16)
-        chan = 8 * np.arange(g) + phase
-        ref = np.zeros((B, HKV * g))
-        for b in range(B):
-            for j in range(HKV):
-                e = 126 - int(exps[8 * b + j])
-                for i in range(g):
-                    q[b, j * g + i, chan[i]] = (e + 127) << 7
-                    ref[b, j * g + i] = float(np.float32(SCALE)) * 2.0 ** e * k_dec[b, j, chan[i]]
-        d.q = torch.from_numpy(q.view(np.int16)).cuda()
-        _, lse = d.attn(use_bf16_pools=mixed_kernel)
-        got = lse.cpu().numpy().astype(np.float64)
-        err = np.abs(got - ref)
-        bad = np.argwhere(err > 1e-6 * np.abs(ref))
-        assert bad.size == 0, (f"phase {phase}: {len(bad)} mismatches; first (b, h) "
-                               f"{bad[:4].tolist()} got {got[tuple(bad[0])]} ref {ref[tuple(bad[0])]}")
+    for half in (0, 1):
+        note(f"attn decode routes: K exhaustive, B={B} half={half}, mixed-format kernel={mixed_kernel}")
+        rng = np.random.default_rng(21 + half)
+        kv, ids, exps = _kv(rng, B, HKV * g, "k", half)
+        k_dec = oracle.bf16_to_f64(kv.k_bf16[ids, :, 0, :])      # [B][Hkv][D]
+        d = DevKV(kv)
+        for phase in range(8):
+            # head h of group j probes channel 8 (h % 16) + phase with weight 2^(126 - E)
+            q = np.zeros((B, HKV * g, D), np.uint16)
+            chan = 8 * np.arange(g) + phase
+            ref = np.zeros((B, HKV * g))
+            for b in range(B):
+                for j in range(HKV):
+                    e = 126 - int(exps[8 * b + j])
+                    q[b, j * g + np.arange(g), chan] = (e + 127) << 7
+                    ref[b, j * g: (j + 1) * g] = float(np.float32(SCALE)) * 2.0 ** e * k_dec[b, j, chan]
+            d.q = torch.from_numpy(q.view(np.int16)).cuda()
+            _, lse = d.attn(use_bf16_pools=mixed_kernel)
+            got = lse.cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref)
+            bad = np.argwhere(err > 1e-6 * np.abs(ref))
+            assert bad.size == 0, (f"half {half} phase {phase}: {len(bad)} mismatches; first (b, h) "
+                                   f"{bad[:4].tolist()} got {got[tuple(bad[0])]} ref {ref[tuple(bad[0])]}")
