@@ -493,12 +493,14 @@ __device__ __forceinline__ void process_page(const PageRaw<MIXED> &c, const Page
 
 // ------------------------------------------------------------------ kernel
 
-// LDS bytes of the wave merge: (WAVES - 1) partial accumulators of 32 x 64
-// floats, then the waves' (max, sum) per head.
+// LDS bytes of the wave merge: WAVES - 1 slots of accumulators, then their
+// (max, sum) per head.
+constexpr int kMergeSlotBytes = 8 * 64 * 16;     // one wave's accumulators: 8 x f32x4 per lane
+
 template <int WAVES>
 constexpr int merge_bytes()
 {
-    return ((WAVES - 1) * 32 * 64 + 2 * WAVES * 16) * 4;
+    return (WAVES - 1) * (kMergeSlotBytes + 16 * 8);
 }
 
 // With 8 waves per workgroup (one workgroup per CU), waves 0..3 are issued
@@ -622,50 +624,47 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
     // every wave has its partial before the workgroup merge
     __syncthreads();
 
-    // ---- merge the four waves of the workgroup through LDS
-    float l_run = st.l;
-    l_run += __shfl_xor(l_run, 16);
-    l_run += __shfl_xor(l_run, 32);
-    float(*sm_o)[32][64] = reinterpret_cast<float(*)[32][64]>(sm_buf);
-    float(*sm_m)[16] = reinterpret_cast<float(*)[16]>(sm_buf + (WAVES - 1) * 32 * 64 * 4);
-    float(*sm_l)[16] = reinterpret_cast<float(*)[16]>(sm_buf + ((WAVES - 1) * 32 * 64 + WAVES * 16) * 4);
-    if (wave > 0) {
-        if (G == 0) {
-            sm_m[wave][r] = st.m;
-            sm_l[wave][r] = l_run;
-        }
-#pragma unroll
-        for (int n = 0; n < 8; n++)
-#pragma unroll
-            for (int i = 0; i < 4; i++)
-                sm_o[wave - 1][8 * i + n][lane] = O[n][i];
-    }
-    __syncthreads();
-    if (wave > 0)
-        return;
-
+    // ---- merge the waves of the workgroup through LDS, as a fixed binary
+    //      tree (waves h..2h-1 hand their partial to waves 0..h-1), so every
+    //      wave takes part and the result does not depend on timing
+    float L = st.l;
+    L += __shfl_xor(L, 16);
+    L += __shfl_xor(L, 32);
     float M = st.m;
+    f32x4_t *sm_o = reinterpret_cast<f32x4_t *>(sm_buf);
+    float2 *sm_ml = reinterpret_cast<float2 *>(sm_buf + (WAVES - 1) * kMergeSlotBytes);
 #pragma unroll
-    for (int w = 1; w < WAVES; w++)
-        M = fmaxf(M, sm_m[w][r]);
-    float L;
-    {
-        const float a0 = __builtin_amdgcn_exp2f(st.m - M);
-        L = l_run * a0;
-#pragma unroll
-        for (int n = 0; n < 8; n++)
-            O[n] *= a0;
-#pragma unroll
-        for (int w = 1; w < WAVES; w++) {
-            const float aw = __builtin_amdgcn_exp2f(sm_m[w][r] - M);
-            L = fmaf(aw, sm_l[w][r], L);
+    for (int h = WAVES / 2; h >= 1; h /= 2) {
+        const int slot_base = WAVES - 2 * h;     // each level has its own slots: one barrier per level
+        if (wave >= h && wave < 2 * h) {
+            const int slot = slot_base + wave - h;
 #pragma unroll
             for (int n = 0; n < 8; n++)
+                sm_o[(slot * 8 + n) * 64 + lane] = O[n];
+            if (G == 0)
+                sm_ml[slot * 16 + r] = float2{M, L};
+        }
+        __syncthreads();
+        if (wave < h) {
+            const int slot = slot_base + wave;
+            const float2 ml = sm_ml[slot * 16 + r];
+            const float Mn = fmaxf(M, ml.x);
+            const float Ms = Mn == -INFINITY ? 0.0f : Mn;     // two empty partials stay empty
+            const float ca = __builtin_amdgcn_exp2f(M - Ms);
+            const float cb = __builtin_amdgcn_exp2f(ml.x - Ms);
+            L = fmaf(L, ca, ml.y * cb);
+            M = Mn;
+#pragma unroll
+            for (int n = 0; n < 8; n++) {
+                const f32x4_t ob = sm_o[(slot * 8 + n) * 64 + lane];
 #pragma unroll
                 for (int i = 0; i < 4; i++)
-                    O[n][i] = fmaf(aw, sm_o[w - 1][8 * i + n][lane], O[n][i]);
+                    O[n][i] = fmaf(O[n][i], ca, ob[i] * cb);
+            }
         }
     }
+    if (wave > 0)
+        return;
 
     if (n_split_b == 1) {
         if (head_ok) {
