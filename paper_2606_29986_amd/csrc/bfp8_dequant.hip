@@ -54,7 +54,8 @@ __global__ __launch_bounds__(64 * kDequantWaves) void bfp8_dequant_pages_kernel(
         const int es = (int)ex[s] - kExpBias;
         const u32x2_t a = bfp8_word_to_bf16(w[s].x, es);
         const u32x2_t c = bfp8_word_to_bf16(w[s].y, es);
-        *reinterpret_cast<u32x4_t *>(o + 8 * run) = u32x4_t{a.x, a.y, c.x, c.y};
+        // streaming store: the rebuilt pages are not read again by this pass
+        __builtin_nontemporal_store(u32x4_t{a.x, a.y, c.x, c.y}, reinterpret_cast<u32x4_t *>(o + 8 * run));
     }
 }
 

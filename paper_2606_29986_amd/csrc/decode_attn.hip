@@ -129,6 +129,7 @@ __device__ __forceinline__ void store_out_row(uint16_t *dst, const f32x4_t (&o)[
 struct PageInfo {
     uint32_t ent;
     int nval;
+    bool live;      // false: a prefetch past the wave's last page (loads fetch nothing)
 };
 
 __device__ __forceinline__ PageInfo page_info(const uint32_t *sm_pt, int pi, int n_tok)
@@ -136,6 +137,7 @@ __device__ __forceinline__ PageInfo page_info(const uint32_t *sm_pt, int pi, int
     PageInfo c;
     c.nval = min(kPageSize, n_tok - pi * kPageSize);
     c.ent = __builtin_amdgcn_readfirstlane(sm_pt[pi]);
+    c.live = true;
     return c;
 }
 
@@ -197,10 +199,14 @@ __device__ __forceinline__ void load_page_regs(PageRaw<false> &c, const PageInfo
                                                int j, const LaneOffsets &o)
 {
     const int64_t tile = (int64_t)(inf.ent & kIdMask) * p.hkv + j;
-    const __amdgpu_buffer_rsrc_t kt = tile_rsrc(p.k_mant + tile * kTileMant, kTileMant);
-    const __amdgpu_buffer_rsrc_t kx = tile_rsrc(p.k_exp + tile * kTileExp, kTileExp);
-    const __amdgpu_buffer_rsrc_t vt = tile_rsrc(p.v_mant + tile * kTileMant, kTileMant);
-    const __amdgpu_buffer_rsrc_t vx = tile_rsrc(p.v_exp + tile * kTileExp, kTileExp);
+    // a prefetch past the wave's last page gets empty resources: its loads
+    // are issued (so the wait counts stay uniform) but read no memory
+    const uint32_t mant_bytes = inf.live ? kTileMant : 0u;
+    const uint32_t exp_bytes = inf.live ? kTileExp : 0u;
+    const __amdgpu_buffer_rsrc_t kt = tile_rsrc(p.k_mant + tile * kTileMant, mant_bytes);
+    const __amdgpu_buffer_rsrc_t kx = tile_rsrc(p.k_exp + tile * kTileExp, exp_bytes);
+    const __amdgpu_buffer_rsrc_t vt = tile_rsrc(p.v_mant + tile * kTileMant, mant_bytes);
+    const __amdgpu_buffer_rsrc_t vx = tile_rsrc(p.v_exp + tile * kTileExp, exp_bytes);
     c.km0 = __builtin_amdgcn_raw_buffer_load_b128(kt, o.k0, 0, kStream);
     c.km1 = __builtin_amdgcn_raw_buffer_load_b128(kt, o.k1, 0, kStream);
     c.ke = __builtin_amdgcn_raw_buffer_load_b64(kx, o.ke, 0, kStream);
@@ -598,13 +604,16 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
     // Register pipeline: the loads of the wave's next page are issued before
     // the current page is decoded and multiplied, so one page per wave is in
     // flight behind the computation (two register sets, alternating).  Past
-    // the wave's last page the prefetch re-requests that page (a cache hit),
-    // so the loop has no branch between a load and its use.
+    // the wave's last page the prefetch is still issued (over empty buffer
+    // resources on the pure-BFP8 path; re-requesting the last page on the
+    // mixed path), so the loop has no branch between a load and its use.
     const WavePages wp = wave_pages<WAVES>(n_pages, wave);
     const int my_pages = wp.count;
     if (my_pages > 0) {
         auto page_at = [&](int k) {
-            return page_info(sm_pt, wp.first + min(k, my_pages - 1) * 4, n_tok);
+            PageInfo c = page_info(sm_pt, wp.first + min(k, my_pages - 1) * 4, n_tok);
+            c.live = k < my_pages;
+            return c;
         };
         const LaneOffsets lo = lane_offsets(G, r);
         PageRaw<MIXED> c0, c1;
