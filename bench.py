@@ -133,6 +133,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--kv-format", choices=["bfp8", "bf16"], default="bfp8",
+                    help="bf16: every page is already BF16 and the step is attention only "
+                         "(the dequant-free baseline)")
     ap.add_argument("--resident-layers", type=int, default=0,
                     help="layers kept resident (0 = all that the workload defines, 8 for the trace mix)")
     args = ap.parse_args()
@@ -154,15 +157,21 @@ def main():
     pt_np, total_pages = wl.page_table(w, ctx)
     max_ctx = int(ctx.max())
     mixed = w.bf16_page_fraction > 0
+    all_bf16 = args.kv_format == "bf16"
+    if all_bf16 and mixed:
+        print(json.dumps({"error": "--kv-format bf16 applies to the uniform-format workloads"}))
+        sys.exit(2)
     resident = args.resident_layers or (8 if mixed else w.layers)
     n_pools = 2 * resident
 
     # ---- resident inputs: one allocation per stream, pool p = 2*layer + (0: K, 1: V)
-    mant = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim),
+    # (the all-BF16 baseline never reads BFP8 pools: one page of each stands in)
+    bfp8_pages = 1 if all_bf16 else total_pages
+    mant = torch.empty((n_pools, bfp8_pages, w.num_kv_heads, w.page_size, w.head_dim),
                        dtype=torch.uint8, device=dev)
-    expo = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim // 16),
+    expo = torch.empty((n_pools, bfp8_pages, w.num_kv_heads, w.page_size, w.head_dim // 16),
                        dtype=torch.uint8, device=dev)
-    for layer in range(resident):
+    for layer in range(0 if all_bf16 else resident):
         for kind, off in (("k", 0), ("v", 1)):
             m, e = wl.bfp8_codes_device(w, layer, kind, total_pages, dev)
             mant[2 * layer + off].copy_(m)
@@ -176,7 +185,16 @@ def main():
     ctx_d = torch.from_numpy(ctx).to(dev)
 
     bf16_tokens = 0
-    if mixed:
+    if all_bf16:
+        bf16 = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim),
+                           dtype=torch.int16, device=dev)
+        bf16.random_(-32768, 32767, generator=g)
+        bf16 &= 0x3FFF                       # finite BF16 patterns
+        tagged = pt_np | wl.TAG_BF16
+        pt_d = torch.from_numpy(tagged.astype(np.int32)).to(dev)
+        bf16_tokens = int(ctx.sum())
+        dq_pages = 0
+    elif mixed:
         # BF16 pool per resident layer and stream; tagged pages read it
         mask = wl.bf16_page_mask(w, total_pages)
         bf16 = torch.empty((n_pools, total_pages, w.num_kv_heads, w.page_size, w.head_dim),
@@ -215,8 +233,8 @@ def main():
         hma.decode_attn_bfp8(
             q[layer_slot], mant[2 * layer_slot], expo[2 * layer_slot], mant[2 * layer_slot + 1],
             expo[2 * layer_slot + 1], pt_d, ctx_d, max_ctx, out,
-            k_bf16=bf16[2 * layer_slot] if mixed else None,
-            v_bf16=bf16[2 * layer_slot + 1] if mixed else None,
+            k_bf16=bf16[2 * layer_slot] if (mixed or all_bf16) else None,
+            v_bf16=bf16[2 * layer_slot + 1] if (mixed or all_bf16) else None,
             scale=scale, num_kv_heads=w.num_kv_heads, tokens_per_split=tps, workspace=ws,
             stream=stream)
 
@@ -271,9 +289,10 @@ def main():
             if record and not per_launch:
                 e1 = ev()
                 evs.append(("attn", e0, e1, n_launch))
-            dequant_launch()
-            if record and not per_launch:
-                evs.append(("dq", e1, ev(), 1))
+            if not all_bf16:
+                dequant_launch()
+                if record and not per_launch:
+                    evs.append(("dq", e1, ev(), 1))
         return evs
 
     for _ in range(args.warmup):
@@ -300,7 +319,10 @@ def main():
         single = np.array([e0.elapsed_time(e1) * 1e3 for _, e0, e1, _ in evs])
 
     a_bytes = attn_bytes(w, ctx, bf16_tokens)
-    if mixed:
+    if all_bf16:
+        d_bytes = 0
+        step_bytes = n_launch * a_bytes
+    elif mixed:
         d_bytes = dequant_bytes(w, dq_pages, 2)
         step_bytes = n_launch * (a_bytes + d_bytes)
     else:
@@ -315,7 +337,7 @@ def main():
     try:
         tf = json.load(open(TRAFFIC_FILE))
         ent = tf.get("decode_attn_bfp8", {}).get(w.name)
-        if ent and ent.get("kernel_hash") == kernel_hash(KERNEL_SOURCES[0]):
+        if ent and ent.get("kernel_hash") == kernel_hash(KERNEL_SOURCES[0]) and not all_bf16:
             traffic = ent["bytes_per_launch"]
     except (OSError, ValueError):
         pass
@@ -340,7 +362,11 @@ def main():
             "layers": w.layers, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
             "head_dim": w.head_dim, "page_size": w.page_size, "tokens_per_split": tps,
             "resident_layers": resident, "bf16_page_fraction": w.bf16_page_fraction,
-            "step": ("attention over %d layers (mixed BF16/BFP8 pages) + per-layer rebuild of "
+            "kv_format": "bf16 (every page already BF16)" if all_bf16 else
+                         ("mixed" if mixed else "bfp8"),
+            "step": ("attention over %d layers, every page already BF16 (dequant-free baseline)"
+                     % n_launch) if all_bf16 else
+                    ("attention over %d layers (mixed BF16/BFP8 pages) + per-layer rebuild of "
                      "fresh pages" % n_launch) if mixed else
                     ("attention over %d layers + one launch rebuilding request 0's K/V of all "
                      "%d layers (%d pages each)" % (n_launch, w.layers, dq_pages)),
@@ -350,16 +376,16 @@ def main():
         "attn_us_p99": round(float(np.percentile(single, 99)), 3),
         "attn_GBps": round(attn_gbps, 2),
         "attn_frac_hbm_peak": round(attn_gbps / HBM_PEAK_GBPS, 4),
-        "dequant_us": round(float(dq_us.mean()), 3),
-        "dequant_us_p99": round(float(np.percentile(dq_us, 99)), 3),
-        "dequant_GBps": round(d_bytes / (float(dq_us.mean()) * 1e-6) / 1e9, 2),
+        "dequant_us": round(float(dq_us.mean()), 3) if dq_us.size else None,
+        "dequant_us_p99": round(float(np.percentile(dq_us, 99)), 3) if dq_us.size else None,
+        "dequant_GBps": round(d_bytes / (float(dq_us.mean()) * 1e-6) / 1e9, 2) if dq_us.size else None,
         "roofline": {"bound": "hbm", "achieved": round(attn_gbps, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": traffic,
                      "kernel": "decode_attn_bfp8_kernel",
                      "algorithmic_bytes_per_launch": a_bytes},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not all_bf16:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res), flush=True)
 
