@@ -121,6 +121,82 @@ def copy_probe(mib: int, reps: int = 5) -> None:
     print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n, "reps": reps}))
 
 
+def ingress_experiment(w, ctx, n_requests, attn_launch, resident, stream, steps):
+    """Decode steps (attention over every layer, on `stream`) alone, then
+    while n_requests new requests of the workload's longest context arrive:
+    per layer, their raw BFP8 K and V pages are copied from pinned host
+    memory and rebuilt into a BF16 cache by hma_ingress_rebuild on a side
+    stream (the decode side of the layer-wise transfer pipeline)."""
+    import torch
+    import paper_2606_29986_amd as hma
+    dev = torch.device("cuda", 0)
+    n_pages = int(wl.pages_per_seq(np.array([int(ctx.max())]), w.page_size)[0])
+    shape = (2, n_pages, w.num_kv_heads, w.page_size, w.head_dim)
+    eshape = shape[:-1] + (w.head_dim // 16,)
+    g = torch.Generator().manual_seed(7)
+    host = []
+    for layer in range(w.layers):          # one request's bytes, as the network delivers them
+        m = torch.randint(0, 256, shape, dtype=torch.uint8, generator=g).pin_memory()
+        e = torch.randint(124, 132, eshape, dtype=torch.uint8, generator=g).pin_memory()
+        host.append((m, e))
+    stage_m = torch.empty(shape, dtype=torch.uint8, device=dev)
+    stage_e = torch.empty(eshape, dtype=torch.uint8, device=dev)
+    dst = torch.empty((w.layers,) + shape, dtype=torch.int16, device=dev)
+    side = torch.cuda.Stream(device=dev)
+    req_bytes = w.layers * sum(int(t.numel()) for t in host[0])
+
+    def decode_steps(k):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(k):
+            for layer in range(w.layers):
+                attn_launch(layer % resident)
+        e1.record(stream)
+        return e0, e1
+
+    for _ in range(2):
+        decode_steps(1)
+    torch.cuda.synchronize()
+    a0, a1 = decode_steps(steps)
+    torch.cuda.synchronize()
+    alone = a0.elapsed_time(a1) / steps
+    # ingress alone
+    i0 = torch.cuda.Event(enable_timing=True)
+    i1 = torch.cuda.Event(enable_timing=True)
+    i0.record(side)
+    for layer in range(w.layers):
+        hma.ingress_rebuild(host[layer][0], host[layer][1], stage_m, stage_e, dst[layer], None,
+                            n_pools=2, dst_pool_stride_pages=n_pages,
+                            num_kv_heads=w.num_kv_heads, stream=side)
+    i1.record(side)
+    torch.cuda.synchronize()
+    ingress_alone_ms = i0.elapsed_time(i1)
+    # both: the side stream carries n_requests requests while decode runs
+    side_evs = []
+    s0 = torch.cuda.Event(enable_timing=True)
+    s0.record(side)
+    for _ in range(n_requests):
+        for layer in range(w.layers):
+            hma.ingress_rebuild(host[layer][0], host[layer][1], stage_m, stage_e, dst[layer], None,
+                                n_pools=2, dst_pool_stride_pages=n_pages,
+                                num_kv_heads=w.num_kv_heads, stream=side)
+    s1 = torch.cuda.Event(enable_timing=True)
+    s1.record(side)
+    overlap_steps = max(1, int(n_requests * ingress_alone_ms / alone))
+    b0, b1 = decode_steps(overlap_steps)
+    torch.cuda.synchronize()
+    both = b0.elapsed_time(b1) / overlap_steps
+    return {"requests": n_requests, "request_bytes": req_bytes,
+            "ingress_ms_per_request_alone": round(ingress_alone_ms, 3),
+            "ingress_GBps_alone": round(req_bytes / (ingress_alone_ms * 1e-3) / 1e9, 2),
+            "ingress_ms_total_during_decode": round(s0.elapsed_time(s1), 3),
+            "decode_ms_per_step_alone": round(alone, 4),
+            "decode_ms_per_step_with_ingress": round(both, 4),
+            "decode_steps_overlapped": overlap_steps,
+            "decode_slowdown": round(both / alone - 1.0, 4)}
+
+
 # --------------------------------------------------------------------- main
 
 def main():
@@ -136,6 +212,10 @@ def main():
     ap.add_argument("--kv-format", choices=["bfp8", "bf16"], default="bfp8",
                     help="bf16: every page is already BF16 and the step is attention only "
                          "(the dequant-free baseline)")
+    ap.add_argument("--ingress-requests", type=int, default=0,
+                    help="also measure decode steps while this many new requests' raw BFP8 "
+                         "pages stream in from pinned host memory and are rebuilt on a side "
+                         "stream (hma_ingress_rebuild, one call per layer)")
     ap.add_argument("--resident-layers", type=int, default=0,
                     help="layers kept resident (0 = all that the workload defines, 8 for the trace mix)")
     args = ap.parse_args()
@@ -385,6 +465,9 @@ def main():
                      "kernel": "decode_attn_bfp8_kernel",
                      "algorithmic_bytes_per_launch": a_bytes},
     }
+    if args.ingress_requests and not mixed and not all_bf16:
+        res["ingress"] = ingress_experiment(w, ctx, args.ingress_requests, attn_launch, resident,
+                                            stream, max(args.steps, 10))
     if not args.no_cpu_baseline and not all_bf16:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res), flush=True)

@@ -90,12 +90,13 @@ enum hma_status {
  *              source ranges touched by this call
  *   src_pages, dst_pages  int32 [n_pages] device arrays of page ids (ids in
  *              range of their pools; no two pairs may name the same
- *              destination page)
+ *              destination page); either may be NULL, meaning page i
+ *              itself (the identity)
  *   n_pages    number of page pairs (0 is a no-op)
  *   n_pools    number of pools (>= 1 unless n_pages == 0)
  *   num_kv_heads >= 1, head_dim == 128, page_size == 16
- * Errors: HMA_EINVAL (NULL pointer with n_pages > 0, negative count,
- * misalignment, stride smaller than needed to keep pools apart),
+ * Errors: HMA_EINVAL (NULL pool pointer with n_pages > 0, negative count,
+ * misalignment, pool stride below 1 with n_pools > 1),
  * HMA_EUNSUPPORTED (head_dim / page_size), HMA_EHIP.
  */
 HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst_bf16,
@@ -103,6 +104,38 @@ HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_e
                            int32_t n_pools, int64_t src_pool_stride_pages,
                            int64_t dst_pool_stride_pages, int32_t num_kv_heads,
                            int32_t head_dim, int32_t page_size, void *stream);
+
+/*
+ * hma_ingress_rebuild -- the decode-side end of the layer-wise transfer
+ * pipeline (Sec. 3.2: the decoder overlaps receive, host-to-device copy and
+ * dequantization with decode; Sec. 3.3: raw BFP8 bytes arrive verbatim and are
+ * rebuilt lazily).  On `stream`, in order:
+ *   1. copy n_pools x n_pages raw BFP8 pages (mantissa and exponent streams)
+ *      from host memory into the device staging buffers;
+ *   2. rebuild them into the BF16 pools: staged page i of pool p goes to page
+ *      dst_pages[i] of BF16 pool p (exactly as hma_bfp8_dequant_pages).
+ * Nothing is synchronized: callers run this on a side stream, once per layer
+ * as the layer's bytes arrive, and gate the decode stream on an event
+ * recorded after it.  The staging buffers may be reused by the next call on
+ * the same stream.
+ *
+ *   host_mant  uint8 [n_pools][n_pages][Hkv][16][128]; pinned (page-locked)
+ *              host memory for an asynchronous copy
+ *   host_exp   uint8 [n_pools][n_pages][Hkv][16][8]; pinned
+ *   stage_mant, stage_exp  device buffers of the same sizes, 16-byte aligned
+ *   dst_bf16   uint16 BF16 pool 0, 16-byte aligned; pool p starts
+ *              p * dst_pool_stride_pages pages after it
+ *   dst_pages  int32 [n_pages] device array of destination page ids (NULL:
+ *              page i); no two may repeat
+ *   num_kv_heads >= 1, head_dim == 128, page_size == 16
+ * Errors: HMA_EINVAL (NULL pointer with pages to move, negative count,
+ * misalignment, staging overlapping the destination, pool stride below 1
+ * with n_pools > 1), HMA_EUNSUPPORTED, HMA_EHIP (copy or launch failed).
+ */
+HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,
+                        uint8_t *stage_exp, uint16_t *dst_bf16, const int32_t *dst_pages,
+                        int32_t n_pages, int32_t n_pools, int64_t dst_pool_stride_pages,
+                        int32_t num_kv_heads, int32_t head_dim, int32_t page_size, void *stream);
 
 /*
  * hma_decode_attn_bfp8 -- single-token GQA decode attention over the paged,

@@ -47,6 +47,8 @@ def lib() -> ctypes.CDLL:
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     L.hma_bfp8_dequant_pages.argtypes = [vp, vp, vp, vp, vp, i32, i32, i64, i64, i32, i32, i32, vp]
     L.hma_bfp8_dequant_pages.restype = ctypes.c_int
+    L.hma_ingress_rebuild.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i64, i32, i32, i32, vp]
+    L.hma_ingress_rebuild.restype = ctypes.c_int
     L.hma_decode_attn_bfp8.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, i32,
                                        i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, sz, vp]
     L.hma_decode_attn_bfp8.restype = ctypes.c_int
@@ -116,21 +118,54 @@ def alloc_workspace(batch, num_q_heads, num_kv_heads, max_context_len, tokens_pe
 
 def bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pools=1,
                        src_pool_stride_pages=0, dst_pool_stride_pages=0, num_kv_heads=8,
-                       head_dim=HEAD_DIM, page_size=PAGE_SIZE, stream=None) -> None:
+                       head_dim=HEAD_DIM, page_size=PAGE_SIZE, n_pages=None, stream=None) -> None:
     """hma_bfp8_dequant_pages: rebuild BFP8 pages into the BF16 pool dst_bf16.
 
     src_mant uint8, src_exp uint8, dst_bf16 int16/uint16/bfloat16 device
-    tensors; src_pages / dst_pages int32 device tensors of equal length."""
+    tensors; src_pages / dst_pages int32 device tensors of equal length, or
+    None for the identity (then n_pages gives the count)."""
     _check_dev(src_mant, src_exp, dst_bf16, src_pages, dst_pages)
-    n = int(src_pages.numel()) if not isinstance(src_pages, int) else None
-    if n is None or int(dst_pages.numel()) != n:
-        raise ValueError("src_pages and dst_pages must be tensors of equal length")
+    lens = {int(t.numel()) for t in (src_pages, dst_pages) if t is not None}
+    if n_pages is not None:
+        lens.add(int(n_pages))
+    if len(lens) != 1:
+        raise ValueError("src_pages, dst_pages and n_pages must agree on the page count")
+    n = lens.pop()
     rc = lib().hma_bfp8_dequant_pages(_ptr(src_mant), _ptr(src_exp), _ptr(dst_bf16),
                                       _ptr(src_pages), _ptr(dst_pages), n, n_pools,
                                       src_pool_stride_pages, dst_pool_stride_pages, num_kv_heads,
                                       head_dim, page_size, _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_bfp8_dequant_pages")
+
+
+def ingress_rebuild(host_mant, host_exp, stage_mant, stage_exp, dst_bf16, dst_pages=None,
+                    n_pools=1, dst_pool_stride_pages=0, num_kv_heads=8, head_dim=HEAD_DIM,
+                    page_size=PAGE_SIZE, stream=None) -> None:
+    """hma_ingress_rebuild: copy raw BFP8 pages from host memory to the device
+    staging buffers and rebuild them into the BF16 pools, in order on
+    ``stream``.  host_mant / host_exp are CPU uint8 tensors shaped
+    [n_pools][n_pages][Hkv][16][128] and [...][8] (pinned, for an asynchronous
+    copy); the staging tensors are device tensors of the same sizes."""
+    for t in (host_mant, host_exp):
+        if t.is_cuda or not t.is_contiguous():
+            raise ValueError("host_mant and host_exp must be contiguous CPU tensors")
+    _check_dev(stage_mant, stage_exp, dst_bf16, dst_pages)
+    if host_mant.dim() != 5 or host_exp.dim() != 5:
+        raise ValueError("host buffers are [n_pools][n_pages][Hkv][page_size][...]")
+    pools, n = int(host_mant.shape[0]), int(host_mant.shape[1])
+    if pools != n_pools or host_exp.shape[:2] != host_mant.shape[:2]:
+        raise ValueError("host buffer shapes disagree with n_pools")
+    if stage_mant.numel() < host_mant.numel() or stage_exp.numel() < host_exp.numel():
+        raise ValueError("staging buffers smaller than the host buffers")
+    if dst_pages is not None and int(dst_pages.numel()) != n:
+        raise ValueError("dst_pages must name one page per staged page")
+    rc = lib().hma_ingress_rebuild(host_mant.data_ptr(), host_exp.data_ptr(), _ptr(stage_mant),
+                                   _ptr(stage_exp), _ptr(dst_bf16), _ptr(dst_pages), n, n_pools,
+                                   dst_pool_stride_pages, num_kv_heads, head_dim, page_size,
+                                   _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_ingress_rebuild")
 
 
 def decode_attn_bfp8(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len,

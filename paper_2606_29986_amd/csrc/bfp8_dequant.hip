@@ -32,8 +32,8 @@ __global__ __launch_bounds__(64 * kDequantWaves) void bfp8_dequant_pages_kernel(
     const int64_t rest = tile / hkv;
     const int pair = (int)(rest % n_pages);
     const int64_t pool = rest / n_pages;
-    const int64_t sp = src_pages[pair];
-    const int64_t dp = dst_pages[pair];
+    const int64_t sp = src_pages ? src_pages[pair] : pair;     // NULL: the identity
+    const int64_t dp = dst_pages ? dst_pages[pair] : pair;
     const int64_t src_tile = (pool * src_stride_pages + sp) * hkv + head;
     const int64_t dst_tile = (pool * dst_stride_pages + dp) * hkv + head;
     const uint8_t *m = src_mant + src_tile * kTileMant;
@@ -70,6 +70,20 @@ int launch_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, u
                        0, stream, src_mant, src_exp, dst, src_pages, dst_pages, n_pages, n_tiles,
                        hkv, src_stride_pages, dst_stride_pages);
     return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,
+                           uint8_t *stage_exp, uint16_t *dst, const int32_t *dst_pages, int32_t n_pages,
+                           int32_t n_pools, int64_t dst_stride_pages, int32_t hkv, size_t mant_bytes,
+                           size_t exp_bytes, hipStream_t stream)
+{
+    if (hipMemcpyAsync(stage_mant, host_mant, mant_bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
+        return -1;
+    if (hipMemcpyAsync(stage_exp, host_exp, exp_bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
+        return -1;
+    // staged pool p holds its n_pages pages contiguously: source stride n_pages
+    return launch_bfp8_dequant_pages(stage_mant, stage_exp, dst, nullptr, dst_pages, n_pages, n_pools,
+                                     n_pages, dst_stride_pages, hkv, stream);
 }
 
 }  // namespace hma

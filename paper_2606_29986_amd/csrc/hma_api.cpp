@@ -113,7 +113,7 @@ int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint
         return HMA_EUNSUPPORTED;
     if (n_pages == 0 || n_pools == 0)
         return HMA_OK;
-    if (!src_mant || !src_exp || !dst_bf16 || !src_pages || !dst_pages)
+    if (!src_mant || !src_exp || !dst_bf16)
         return HMA_EINVAL;
     if (!aligned(src_mant, 16) || !aligned(src_exp, 16) || !aligned(dst_bf16, 16))
         return HMA_EINVAL;
@@ -130,6 +130,46 @@ int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint
                                                   n_pages, n_pools, src_pool_stride_pages,
                                                   dst_pool_stride_pages, num_kv_heads,
                                                   static_cast<hipStream_t>(stream));
+    return rc == 0 ? HMA_OK : HMA_EHIP;
+}
+
+int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,
+                        uint8_t *stage_exp, uint16_t *dst_bf16, const int32_t *dst_pages,
+                        int32_t n_pages, int32_t n_pools, int64_t dst_pool_stride_pages,
+                        int32_t num_kv_heads, int32_t head_dim, int32_t page_size, void *stream)
+{
+    if (n_pages < 0 || n_pools < 0 || num_kv_heads <= 0)
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (n_pages == 0 || n_pools == 0)
+        return HMA_OK;
+    if (!host_mant || !host_exp || !stage_mant || !stage_exp || !dst_bf16)
+        return HMA_EINVAL;
+    if (!aligned(stage_mant, 16) || !aligned(stage_exp, 16) || !aligned(dst_bf16, 16))
+        return HMA_EINVAL;
+    if (n_pools > 1 && dst_pool_stride_pages < 1)
+        return HMA_EINVAL;
+    if (dst_pool_stride_pages < 0)
+        return HMA_EINVAL;
+    const int64_t tiles = (int64_t)n_pools * n_pages * num_kv_heads;
+    if (tiles / 4 + 1 > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    const size_t mant_bytes = (size_t)tiles * kSupportedPageSize * kSupportedHeadDim;
+    const size_t exp_bytes = mant_bytes / 16;
+    // the two staging buffers must not overlap each other or start at the
+    // destination (the destination's extent depends on device-side page ids)
+    auto overlaps = [](const void *a, size_t na, const void *b, size_t nb) {
+        const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+        return x < y + nb && y < x + na;
+    };
+    if (overlaps(stage_mant, mant_bytes, stage_exp, exp_bytes))
+        return HMA_EINVAL;
+    if ((const void *)dst_bf16 == (const void *)stage_mant || (const void *)dst_bf16 == (const void *)stage_exp)
+        return HMA_EINVAL;
+    const int rc = hma::launch_ingress_rebuild(host_mant, host_exp, stage_mant, stage_exp, dst_bf16, dst_pages,
+                                               n_pages, n_pools, dst_pool_stride_pages, num_kv_heads,
+                                               mant_bytes, exp_bytes, static_cast<hipStream_t>(stream));
     return rc == 0 ? HMA_OK : HMA_EHIP;
 }
 

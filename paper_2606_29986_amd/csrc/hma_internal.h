@@ -12,11 +12,19 @@ namespace hma {
 constexpr int32_t kMaxTokensPerSplit = 16384;
 constexpr int kMaxSplitPages = kMaxTokensPerSplit / 16;
 
-// Returns 0 on a successful launch, -1 if the launch failed.
+// Returns 0 on a successful launch, -1 if the launch failed.  src_pages or
+// dst_pages may be NULL (identity).
 int launch_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst,
                               const int32_t *src_pages, const int32_t *dst_pages,
                               int32_t n_pages, int32_t n_pools, int64_t src_stride_pages,
                               int64_t dst_stride_pages, int32_t hkv, hipStream_t stream);
+
+// Host -> device copy of the staged pages on `stream`, then their rebuild
+// (src = staged page i, dst = dst_pages[i] or i when NULL).
+int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,
+                           uint8_t *stage_exp, uint16_t *dst, const int32_t *dst_pages, int32_t n_pages,
+                           int32_t n_pools, int64_t dst_stride_pages, int32_t hkv, size_t mant_bytes,
+                           size_t exp_bytes, hipStream_t stream);
 
 struct AttnLaunch {
     const uint16_t *q;

@@ -27,7 +27,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["hma_bfp8_dequant_pages", "hma_decode_attn_bfp8",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
-                            "hma_status_string"])
+                            "hma_ingress_rebuild", "hma_status_string"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -85,13 +85,40 @@ def test_dequant_validation():
     assert _dequant(hkv=0) == hma.HMA_EINVAL
     assert _dequant(D=64) == hma.HMA_EUNSUPPORTED
     assert _dequant(P=32) == hma.HMA_EUNSUPPORTED
-    for k in ("src_mant", "src_exp", "dst", "src_pages", "dst_pages"):
+    # (NULL page lists mean the identity and are valid: not probed here, since
+    # with every other argument valid the call would launch on fake pointers)
+    for k in ("src_mant", "src_exp", "dst"):
         assert _dequant(**{k: None}) == hma.HMA_EINVAL, k
     for k in ("src_mant", "src_exp", "dst"):
         assert _dequant(**{k: MISALIGNED}) == hma.HMA_EINVAL, k
     assert _dequant(dst=FAKE) == hma.HMA_EINVAL           # aliases the source
     assert _dequant(n_pools=2, src_stride=0, dst_stride=4) == hma.HMA_EINVAL
     assert _dequant(n_pools=2, src_stride=4, dst_stride=-1) == hma.HMA_EINVAL
+
+
+def _ingress(**kw):
+    a = dict(hm=FAKE, he=FAKE, sm=FAKE * 2, se=FAKE * 4, dst=FAKE * 8, dst_pages=None, n_pages=4,
+             n_pools=2, dst_stride=64, hkv=8, D=128, P=16)
+    a.update(kw)
+    return hma.lib().hma_ingress_rebuild(a["hm"], a["he"], a["sm"], a["se"], a["dst"], a["dst_pages"],
+                                         a["n_pages"], a["n_pools"], a["dst_stride"], a["hkv"],
+                                         a["D"], a["P"], None)
+
+
+def test_ingress_validation():
+    assert _ingress(n_pages=0, hm=None) == hma.HMA_OK        # nothing to move
+    assert _ingress(n_pools=0) == hma.HMA_OK
+    assert _ingress(n_pages=-1) == hma.HMA_EINVAL
+    assert _ingress(hkv=0) == hma.HMA_EINVAL
+    assert _ingress(D=64) == hma.HMA_EUNSUPPORTED
+    assert _ingress(P=8) == hma.HMA_EUNSUPPORTED
+    for k in ("hm", "he", "sm", "se", "dst"):
+        assert _ingress(**{k: None}) == hma.HMA_EINVAL, k
+    for k in ("sm", "se", "dst"):
+        assert _ingress(**{k: MISALIGNED}) == hma.HMA_EINVAL, k
+    assert _ingress(dst_stride=0) == hma.HMA_EINVAL          # two pools need a stride
+    assert _ingress(se=FAKE * 2 + 64) == hma.HMA_EINVAL      # staging buffers overlap
+    assert _ingress(dst=FAKE * 2) == hma.HMA_EINVAL          # destination is the staging
 
 
 def _attn(**kw):
