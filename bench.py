@@ -507,6 +507,20 @@ def main():
                      "kernel": "decode_attn_bfp8_kernel",
                      "algorithmic_bytes_per_launch": a_bytes},
     }
+    if not mixed and not all_bf16:
+        # the same rebuild through the one-thread-per-element baseline (Sec. 3.3
+        # sets a naive elementwise reconstruction against the fused pass)
+        n0 = torch.cuda.Event(enable_timing=True)
+        n1 = torch.cuda.Event(enable_timing=True)
+        n0.record(stream)
+        hma.bfp8_dequant_pages(mant, expo, bf16_dst, src_d, dst_d, n_pools=n_pools,
+                               src_pool_stride_pages=total_pages, dst_pool_stride_pages=dq_pages,
+                               num_kv_heads=w.num_kv_heads, stream=stream, naive=True)
+        n1.record(stream)
+        torch.cuda.synchronize()
+        naive_us = n0.elapsed_time(n1) * 1e3
+        res["naive_rebuild_us"] = round(naive_us, 1)
+        res["naive_over_fused_rebuild"] = round(naive_us / float(dq_us.mean()), 2)
     if args.ingress_requests and not mixed and not all_bf16:
         res["ingress"] = ingress_experiment(w, ctx, args.ingress_requests, attn_launch, resident,
                                             stream, max(args.steps, 10))

@@ -106,6 +106,20 @@ HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_e
                            int32_t head_dim, int32_t page_size, void *stream);
 
 /*
+ * hma_bfp8_dequant_pages_naive -- the same rebuild with one thread per
+ * element (byte loads, 2-byte stores, the block exponent re-read for every
+ * element): the "naive elementwise reconstruction" the paper compares its
+ * fused pass against (Sec. 3.3).  Arguments, result and errors are those of
+ * hma_bfp8_dequant_pages.  A measurement baseline, not for production use.
+ */
+HMA_API int hma_bfp8_dequant_pages_naive(const uint8_t *src_mant, const uint8_t *src_exp,
+                                 uint16_t *dst_bf16, const int32_t *src_pages,
+                                 const int32_t *dst_pages, int32_t n_pages, int32_t n_pools,
+                                 int64_t src_pool_stride_pages, int64_t dst_pool_stride_pages,
+                                 int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                                 void *stream);
+
+/*
  * hma_ingress_rebuild -- the decode-side end of the layer-wise transfer
  * pipeline (Sec. 3.2: the decoder overlaps receive, host-to-device copy and
  * dequantization with decode; Sec. 3.3: raw BFP8 bytes arrive verbatim and are

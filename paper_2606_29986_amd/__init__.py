@@ -47,6 +47,8 @@ def lib() -> ctypes.CDLL:
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     L.hma_bfp8_dequant_pages.argtypes = [vp, vp, vp, vp, vp, i32, i32, i64, i64, i32, i32, i32, vp]
     L.hma_bfp8_dequant_pages.restype = ctypes.c_int
+    L.hma_bfp8_dequant_pages_naive.argtypes = L.hma_bfp8_dequant_pages.argtypes
+    L.hma_bfp8_dequant_pages_naive.restype = ctypes.c_int
     L.hma_ingress_rebuild.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i64, i32, i32, i32, vp]
     L.hma_ingress_rebuild.restype = ctypes.c_int
     L.hma_decode_attn_bfp8.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, i32,
@@ -118,12 +120,14 @@ def alloc_workspace(batch, num_q_heads, num_kv_heads, max_context_len, tokens_pe
 
 def bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pools=1,
                        src_pool_stride_pages=0, dst_pool_stride_pages=0, num_kv_heads=8,
-                       head_dim=HEAD_DIM, page_size=PAGE_SIZE, n_pages=None, stream=None) -> None:
+                       head_dim=HEAD_DIM, page_size=PAGE_SIZE, n_pages=None, stream=None,
+                       naive=False) -> None:
     """hma_bfp8_dequant_pages: rebuild BFP8 pages into the BF16 pool dst_bf16.
 
     src_mant uint8, src_exp uint8, dst_bf16 int16/uint16/bfloat16 device
     tensors; src_pages / dst_pages int32 device tensors of equal length, or
-    None for the identity (then n_pages gives the count)."""
+    None for the identity (then n_pages gives the count).  naive=True runs
+    hma_bfp8_dequant_pages_naive (one thread per element; a baseline)."""
     _check_dev(src_mant, src_exp, dst_bf16, src_pages, dst_pages)
     lens = {int(t.numel()) for t in (src_pages, dst_pages) if t is not None}
     if n_pages is not None:
@@ -131,12 +135,12 @@ def bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pool
     if len(lens) != 1:
         raise ValueError("src_pages, dst_pages and n_pages must agree on the page count")
     n = lens.pop()
-    rc = lib().hma_bfp8_dequant_pages(_ptr(src_mant), _ptr(src_exp), _ptr(dst_bf16),
-                                      _ptr(src_pages), _ptr(dst_pages), n, n_pools,
-                                      src_pool_stride_pages, dst_pool_stride_pages, num_kv_heads,
-                                      head_dim, page_size, _stream(stream))
+    fn = lib().hma_bfp8_dequant_pages_naive if naive else lib().hma_bfp8_dequant_pages
+    rc = fn(_ptr(src_mant), _ptr(src_exp), _ptr(dst_bf16), _ptr(src_pages), _ptr(dst_pages), n,
+            n_pools, src_pool_stride_pages, dst_pool_stride_pages, num_kv_heads, head_dim,
+            page_size, _stream(stream))
     if rc != HMA_OK:
-        raise HmaError(rc, "hma_bfp8_dequant_pages")
+        raise HmaError(rc, "hma_bfp8_dequant_pages" + ("_naive" if naive else ""))
 
 
 def ingress_rebuild(host_mant, host_exp, stage_mant, stage_exp, dst_bf16, dst_pages=None,

@@ -72,6 +72,48 @@ int launch_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, u
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// Comparison baseline for the rebuild above: one thread per element, byte
+// loads and 2-byte stores, no vector access and no sharing of the exponent
+// between the elements of a block -- the "naive elementwise reconstruction"
+// the paper sets against its fused pass (Sec. 3.3).  Same output.
+__global__ __launch_bounds__(256) void bfp8_dequant_pages_naive_kernel(
+    const uint8_t *__restrict__ src_mant, const uint8_t *__restrict__ src_exp,
+    uint16_t *__restrict__ dst, const int32_t *__restrict__ src_pages,
+    const int32_t *__restrict__ dst_pages, int32_t n_pages, int64_t n_elems, int32_t hkv,
+    int64_t src_stride_pages, int64_t dst_stride_pages)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n_elems)
+        return;
+    const int within = (int)(e % kTileMant);            // token * 128 + channel
+    const int64_t tile_idx = e / kTileMant;
+    const int head = (int)(tile_idx % hkv);
+    const int64_t rest = tile_idx / hkv;
+    const int pair = (int)(rest % n_pages);
+    const int64_t pool = rest / n_pages;
+    const int64_t sp = src_pages ? src_pages[pair] : pair;
+    const int64_t dp = dst_pages ? dst_pages[pair] : pair;
+    const int64_t src_tile = (pool * src_stride_pages + sp) * hkv + head;
+    const int64_t dst_tile = (pool * dst_stride_pages + dp) * hkv + head;
+    const uint32_t b = src_mant[src_tile * kTileMant + within];
+    const int E = src_exp[src_tile * kTileExp + (within / kHeadDim) * kExpPerRow + (within % kHeadDim) / kBlock];
+    const float v = __builtin_amdgcn_ldexpf((float)(b & 0x7Fu), E - kExpBias);
+    dst[dst_tile * kTileMant + within] = (uint16_t)((__float_as_uint(v) >> 16) | ((b & 0x80u) << 8));
+}
+
+int launch_bfp8_dequant_pages_naive(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst,
+                                    const int32_t *src_pages, const int32_t *dst_pages,
+                                    int32_t n_pages, int32_t n_pools, int64_t src_stride_pages,
+                                    int64_t dst_stride_pages, int32_t hkv, hipStream_t stream)
+{
+    const int64_t n_elems = (int64_t)n_pools * n_pages * hkv * kTileMant;
+    const int64_t blocks = (n_elems + 255) / 256;
+    hipLaunchKernelGGL(bfp8_dequant_pages_naive_kernel, dim3((unsigned)blocks), dim3(256), 0, stream,
+                       src_mant, src_exp, dst, src_pages, dst_pages, n_pages, n_elems, hkv,
+                       src_stride_pages, dst_stride_pages);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,
                            uint8_t *stage_exp, uint16_t *dst, const int32_t *dst_pages, int32_t n_pages,
                            int32_t n_pools, int64_t dst_stride_pages, int32_t hkv, size_t mant_bytes,

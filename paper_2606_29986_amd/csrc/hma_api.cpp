@@ -78,6 +78,45 @@ int32_t splits_for(int32_t max_ctx, int32_t tps)
     return max_ctx <= 0 ? 1 : (int32_t)(((int64_t)max_ctx + tps - 1) / tps);
 }
 
+int dequant_checked(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst_bf16,
+                    const int32_t *src_pages, const int32_t *dst_pages, int32_t n_pages,
+                    int32_t n_pools, int64_t src_pool_stride_pages, int64_t dst_pool_stride_pages,
+                    int32_t num_kv_heads, int32_t head_dim, int32_t page_size, void *stream,
+                    bool naive)
+{
+    if (n_pages < 0 || n_pools < 0 || num_kv_heads <= 0)
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (n_pages == 0 || n_pools == 0)
+        return HMA_OK;
+    if (!src_mant || !src_exp || !dst_bf16)
+        return HMA_EINVAL;
+    if (!aligned(src_mant, 16) || !aligned(src_exp, 16) || !aligned(dst_bf16, 16))
+        return HMA_EINVAL;
+    if ((const void *)dst_bf16 == (const void *)src_mant || (const void *)dst_bf16 == (const void *)src_exp)
+        return HMA_EINVAL;
+    if (n_pools > 1 && (src_pool_stride_pages < 1 || dst_pool_stride_pages < 1))
+        return HMA_EINVAL;
+    if (src_pool_stride_pages < 0 || dst_pool_stride_pages < 0)
+        return HMA_EINVAL;
+    const int64_t tiles = (int64_t)n_pools * n_pages * num_kv_heads;
+    if (tiles / 4 + 1 > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    if (naive && (tiles * kSupportedPageSize * kSupportedHeadDim + 255) / 256 > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const int rc = naive ? hma::launch_bfp8_dequant_pages_naive(src_mant, src_exp, dst_bf16, src_pages,
+                                                                dst_pages, n_pages, n_pools,
+                                                                src_pool_stride_pages,
+                                                                dst_pool_stride_pages, num_kv_heads, s)
+                         : hma::launch_bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages,
+                                                          dst_pages, n_pages, n_pools,
+                                                          src_pool_stride_pages,
+                                                          dst_pool_stride_pages, num_kv_heads, s);
+    return rc == 0 ? HMA_OK : HMA_EHIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -107,30 +146,20 @@ int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint
                            int64_t dst_pool_stride_pages, int32_t num_kv_heads,
                            int32_t head_dim, int32_t page_size, void *stream)
 {
-    if (n_pages < 0 || n_pools < 0 || num_kv_heads <= 0)
-        return HMA_EINVAL;
-    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
-        return HMA_EUNSUPPORTED;
-    if (n_pages == 0 || n_pools == 0)
-        return HMA_OK;
-    if (!src_mant || !src_exp || !dst_bf16)
-        return HMA_EINVAL;
-    if (!aligned(src_mant, 16) || !aligned(src_exp, 16) || !aligned(dst_bf16, 16))
-        return HMA_EINVAL;
-    if ((const void *)dst_bf16 == (const void *)src_mant || (const void *)dst_bf16 == (const void *)src_exp)
-        return HMA_EINVAL;
-    if (n_pools > 1 && (src_pool_stride_pages < 1 || dst_pool_stride_pages < 1))
-        return HMA_EINVAL;
-    if (src_pool_stride_pages < 0 || dst_pool_stride_pages < 0)
-        return HMA_EINVAL;
-    const int64_t tiles = (int64_t)n_pools * n_pages * num_kv_heads;
-    if (tiles / 4 + 1 > (int64_t)INT_MAX)
-        return HMA_EINVAL;
-    const int rc = hma::launch_bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages,
-                                                  n_pages, n_pools, src_pool_stride_pages,
-                                                  dst_pool_stride_pages, num_kv_heads,
-                                                  static_cast<hipStream_t>(stream));
-    return rc == 0 ? HMA_OK : HMA_EHIP;
+    return dequant_checked(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pages, n_pools,
+                           src_pool_stride_pages, dst_pool_stride_pages, num_kv_heads, head_dim,
+                           page_size, stream, false);
+}
+
+int hma_bfp8_dequant_pages_naive(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst_bf16,
+                                 const int32_t *src_pages, const int32_t *dst_pages, int32_t n_pages,
+                                 int32_t n_pools, int64_t src_pool_stride_pages,
+                                 int64_t dst_pool_stride_pages, int32_t num_kv_heads,
+                                 int32_t head_dim, int32_t page_size, void *stream)
+{
+    return dequant_checked(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pages, n_pools,
+                           src_pool_stride_pages, dst_pool_stride_pages, num_kv_heads, head_dim,
+                           page_size, stream, true);
 }
 
 int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,

@@ -19,6 +19,12 @@ int launch_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, u
                               int32_t n_pages, int32_t n_pools, int64_t src_stride_pages,
                               int64_t dst_stride_pages, int32_t hkv, hipStream_t stream);
 
+// One thread per element: the comparison baseline (same arguments and result).
+int launch_bfp8_dequant_pages_naive(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst,
+                                    const int32_t *src_pages, const int32_t *dst_pages,
+                                    int32_t n_pages, int32_t n_pools, int64_t src_stride_pages,
+                                    int64_t dst_stride_pages, int32_t hkv, hipStream_t stream);
+
 // Host -> device copy of the staged pages on `stream`, then their rebuild
 // (src = staged page i, dst = dst_pages[i] or i when NULL).
 int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,

@@ -25,7 +25,8 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    assert names == sorted(["hma_bfp8_dequant_pages", "hma_decode_attn_bfp8",
+    assert names == sorted(["hma_bfp8_dequant_pages", "hma_bfp8_dequant_pages_naive",
+                            "hma_decode_attn_bfp8",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
                             "hma_ingress_rebuild", "hma_status_string"])
 
@@ -68,17 +69,23 @@ def test_split_and_workspace_queries():
     assert hma.tokens_per_split(4, 30, 8, 512) == 0
 
 
-def _dequant(**kw):
+def _dequant(naive=False, **kw):
     a = dict(src_mant=FAKE, src_exp=FAKE, dst=FAKE * 2, src_pages=FAKE, dst_pages=FAKE,
              n_pages=4, n_pools=1, src_stride=0, dst_stride=0, hkv=8, D=128, P=16)
     a.update(kw)
-    return hma.lib().hma_bfp8_dequant_pages(a["src_mant"], a["src_exp"], a["dst"], a["src_pages"],
+    fn = hma.lib().hma_bfp8_dequant_pages_naive if naive else hma.lib().hma_bfp8_dequant_pages
+    return fn(a["src_mant"], a["src_exp"], a["dst"], a["src_pages"],
                                             a["dst_pages"], a["n_pages"], a["n_pools"],
                                             a["src_stride"], a["dst_stride"], a["hkv"], a["D"],
                                             a["P"], None)
 
 
-def test_dequant_validation():
+@pytest.mark.parametrize("naive", [False, True])
+def test_dequant_validation(naive):
+    _dequant_validation(lambda **kw: _dequant(naive=naive, **kw))
+
+
+def _dequant_validation(_dequant):
     assert _dequant(n_pages=0) == hma.HMA_OK             # no-op, nothing touched
     assert _dequant(n_pools=0) == hma.HMA_OK
     assert _dequant(n_pages=-1) == hma.HMA_EINVAL

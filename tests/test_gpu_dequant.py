@@ -18,7 +18,7 @@ SENTINEL = 0x5A5A
 
 
 def _run(src_mant, src_exp, n_dst_pages_per_pool, src_pages, dst_pages, n_pools, src_stride,
-         dst_stride, hkv):
+         dst_stride, hkv, naive=False):
     dm = dev(src_mant)
     de = dev(src_exp)
     dst = torch.full((n_pools * n_dst_pages_per_pool if n_pools > 1 else n_dst_pages_per_pool,
@@ -26,7 +26,7 @@ def _run(src_mant, src_exp, n_dst_pages_per_pool, src_pages, dst_pages, n_pools,
     hma.bfp8_dequant_pages(dm, de, dst, dev(np.asarray(src_pages, np.int32)),
                            dev(np.asarray(dst_pages, np.int32)), n_pools=n_pools,
                            src_pool_stride_pages=src_stride, dst_pool_stride_pages=dst_stride,
-                           num_kv_heads=hkv)
+                           num_kv_heads=hkv, naive=naive)
     torch.cuda.synchronize()
     return dst.cpu().numpy().view(np.uint16)
 
@@ -38,14 +38,16 @@ def _oracle(src_mant, src_exp, n_dst, src_pages, dst_pages, n_pools, src_stride,
     return ref
 
 
-def test_dequant_exhaustive_table():
-    """All 65,536 (exponent, byte) pairs: 4096 blocks of 16 = 4 pages of 8 heads."""
-    note("dequant: exhaustive (E, byte) table")
+@pytest.mark.parametrize("naive", [False, True])
+def test_dequant_exhaustive_table(naive):
+    """All 65,536 (exponent, byte) pairs: 4096 blocks of 16 = 4 pages of 8 heads
+    (also through the one-thread-per-element baseline)."""
+    note(f"dequant: exhaustive (E, byte) table, naive={naive}")
     E = np.repeat(np.arange(256, dtype=np.uint8), 256)
     B = np.tile(np.arange(256, dtype=np.uint8), 256)
     mant = B.reshape(4, 8, 16, 128)
     exps = E.reshape(4096, 16)[:, 0].reshape(4, 8, 16, 8).copy()
-    got = _run(mant, exps, 4, [0, 1, 2, 3], [0, 1, 2, 3], 1, 0, 0, 8)
+    got = _run(mant, exps, 4, [0, 1, 2, 3], [0, 1, 2, 3], 1, 0, 0, 8, naive=naive)
     want = oracle.decode_blocks(mant, exps).reshape(got.shape)
     bad = np.argwhere(got != want)
     assert bad.size == 0, f"{len(bad)} mismatches, first {bad[:4].tolist()}"
@@ -67,7 +69,8 @@ def test_dequant_smoke_workload_subset_of_pages():
         assert (got[untouched] == SENTINEL).all()
 
 
-def test_dequant_multi_pool_strides_and_ragged_counts():
+@pytest.mark.parametrize("naive", [False, True])
+def test_dequant_multi_pool_strides_and_ragged_counts(naive):
     r = np.random.default_rng(9)
     for n_pools, n_src, n_dst, n_pairs, hkv in ((3, 7, 11, 5, 8), (1, 1, 1, 1, 1), (5, 9, 9, 9, 2),
                                                  (2, 33, 40, 31, 4)):
@@ -76,7 +79,7 @@ def test_dequant_multi_pool_strides_and_ragged_counts():
         ex = r.integers(0, 256, size=(n_pools * n_src, hkv, 16, 8), dtype=np.uint8)
         src = r.choice(n_src, size=n_pairs, replace=False).astype(np.int32)
         dst = r.choice(n_dst, size=n_pairs, replace=False).astype(np.int32)
-        got = _run(mant, ex, n_dst, src, dst, n_pools, n_src, n_dst, hkv)
+        got = _run(mant, ex, n_dst, src, dst, n_pools, n_src, n_dst, hkv, naive=naive)
         want = _oracle(mant, ex, n_dst, src, dst, n_pools, n_src, n_dst, hkv)
         assert np.array_equal(got, want)
 
