@@ -81,6 +81,9 @@ def lib():
         L.ora_dequant_pages.argtypes = [_p(u8), _p(u8), _p(u16), _p(i32), _p(i32), i32, i32,
                                         i64, i64, i32, i32, i32]
         L.ora_dequant_pages.restype = None
+        L.ora_rebuild_tiled.argtypes = [_p(u8), i64, i32, i32, i32, i32, i32, i32, i32, _p(u16),
+                                        _p(i32), i64]
+        L.ora_rebuild_tiled.restype = None
         L.ora_merge_partials.argtypes = [i32, _p(f64), _p(f64), _p(f64), i32, _p(f64), _p(f64)]
         L.ora_merge_partials.restype = None
         L.ora_decode_attn.argtypes = [_p(u16), _p(u8), _p(u8), _p(u8), _p(u8), _p(u16), _p(u16),
@@ -183,6 +186,28 @@ def dequant_pages(src_mant, src_exp, dst, src_pages, dst_pages, n_pools,
                             _ptr(dp, ctypes.c_int32), sp.size, n_pools,
                             src_pool_stride_pages, dst_pool_stride_pages,
                             num_kv_heads, head_dim, page_size)
+    return dst
+
+
+TILE_BYTES = 64 + 32 * 32     # one 32x32 BFP8 tile of a prefill shard
+
+
+def tiled_shard_bytes(n_tokens, heads_per_shard, head_dim=128):
+    """Bytes of one shard: heads x ceil(tokens/32) x head_dim/32 tiles."""
+    return heads_per_shard * ((n_tokens + 31) // 32) * (head_dim // 32) * TILE_BYTES
+
+
+def rebuild_tiled(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens, num_kv_heads, dst,
+                  dst_pages, dst_pool_stride_pages, rope_reorder, head_dim=128, page_size=16):
+    """Tiled prefill shards -> BF16 pages (``dst`` modified in place); see
+    ora_rebuild_tiled for the tile byte order."""
+    assert dst.dtype == np.uint16 and dst.flags["C_CONTIGUOUS"]
+    s = _c(src, np.uint8)
+    dp = _c(dst_pages, np.int32)
+    lib().ora_rebuild_tiled(_ptr(s, ctypes.c_uint8), src_pool_stride_bytes, n_pools, n_shards,
+                            n_tokens, num_kv_heads, head_dim, page_size, int(bool(rope_reorder)),
+                            _ptr(dst, ctypes.c_uint16), _ptr(dp, ctypes.c_int32),
+                            dst_pool_stride_pages)
     return dst
 
 

@@ -220,6 +220,54 @@ void ora_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t
         }
 }
 
+/* ------------------------------------- tiled shards -> BF16 pages */
+
+/* The decoder's single reconstruction pass also turns the prefill side's
+ * tiled layout into row-major pages, merges the per-chip KV shards, and
+ * moves keys from the interleaved rotary order to the half-split order
+ * [Sec. 3.3; Sec. 2.3: the prefill chips work on 32x32 tiles].  The paper
+ * gives no byte order for the tiles; the order used here is:
+ *   shard t (chip t of n_shards) holds KV heads [t*Hs, (t+1)*Hs), Hs = Hkv/n_shards;
+ *   a shard is tiles [local head h][token tile (32 tokens)][channel tile (32 channels)];
+ *   a tile is 64 exponent bytes [face][row] followed by 1024 mantissa bytes
+ *   [face][row][16]; face f covers tile rows 16*(f/2).. and tile channels
+ *   16*(f%2)..; the 16 channels of one face row (one token) share an exponent.
+ * Keys leave the prefill side with rotary pairs (2i, 2i+1); the decode side
+ * pairs (i, i + D/2).  With rope_reorder set, source channel c lands at c/2
+ * (c even) or D/2 + c/2 (c odd); values are untouched.
+ * Pool `pool` of the source starts src_pool_stride_bytes after pool 0; its
+ * shards follow each other.  Token p of the request (p < n_tokens) lands in
+ * slot p % P of page dst_pages[p / P] of BF16 pool `pool`, KV head t*Hs + h. */
+void ora_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                       int32_t n_shards, int32_t n_tokens, int32_t num_kv_heads, int32_t head_dim,
+                       int32_t page_size, int32_t rope_reorder, uint16_t *dst,
+                       const int32_t *dst_pages, int64_t dst_pool_stride_pages)
+{
+    const int32_t hs = num_kv_heads / n_shards;
+    const int32_t token_tiles = (n_tokens + 31) / 32;
+    const int32_t chan_tiles = head_dim / 32;
+    const int64_t tile_bytes = 64 + 32 * 32;
+    const int64_t shard_bytes = (int64_t)hs * token_tiles * chan_tiles * tile_bytes;
+    #pragma omp parallel for collapse(3) schedule(static)
+    for (int32_t pool = 0; pool < n_pools; pool++)
+        for (int32_t t = 0; t < n_shards; t++)
+            for (int32_t h = 0; h < hs; h++)
+                for (int32_t p = 0; p < n_tokens; p++)
+                    for (int32_t c = 0; c < head_dim; c++) {
+                        const int64_t tile_index = ((int64_t)h * token_tiles + p / 32) * chan_tiles + c / 32;
+                        const uint8_t *tile = src + pool * src_pool_stride_bytes + t * shard_bytes
+                                              + tile_index * tile_bytes;
+                        const int rr = p % 32, cc = c % 32;
+                        const int face = (rr / 16) * 2 + cc / 16;
+                        const uint8_t E = tile[face * 16 + rr % 16];
+                        const uint8_t byte = tile[64 + face * 256 + (rr % 16) * 16 + cc % 16];
+                        const int c_out = rope_reorder ? (c % 2 == 0 ? c / 2 : head_dim / 2 + c / 2) : c;
+                        const int64_t page = pool * dst_pool_stride_pages + dst_pages[p / page_size];
+                        const int64_t row = (page * num_kv_heads + (int64_t)t * hs + h) * page_size + p % page_size;
+                        dst[row * head_dim + c_out] = ora_bfp8_decode_value(E, byte);
+                    }
+}
+
 /* ----------------------------------------------------- paged attention */
 
 typedef struct {
