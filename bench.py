@@ -521,6 +521,29 @@ def main():
         naive_us = n0.elapsed_time(n1) * 1e3
         res["naive_rebuild_us"] = round(naive_us, 1)
         res["naive_over_fused_rebuild"] = round(naive_us / float(dq_us.mean()), 2)
+        # the same request from tiled per-chip shards (4 prefill chips), keys
+        # re-laid out from interleaved to half-split rotary order
+        n_req_tok = int(ctx[0])
+        shards = 4 if w.num_kv_heads % 4 == 0 else 1
+        pool_bytes = shards * hma.tiled_shard_bytes(n_req_tok, w.num_kv_heads // shards)
+        tiled_src = torch.randint(0, 256, (2, resident, pool_bytes), dtype=torch.uint8, device=dev)
+        t_us = []
+        for _ in range(3):
+            t0_ = torch.cuda.Event(enable_timing=True)
+            t1_ = torch.cuda.Event(enable_timing=True)
+            t0_.record(stream)
+            for kind in (0, 1):
+                hma.bfp8_rebuild_tiled(tiled_src[kind], bf16_dst[kind], n_req_tok, shards,
+                                       n_pools=resident, src_pool_stride_bytes=pool_bytes,
+                                       dst_pool_stride_pages=2 * dq_pages, rope_reorder=(kind == 0),
+                                       num_kv_heads=w.num_kv_heads, stream=stream)
+            t1_.record(stream)
+            torch.cuda.synchronize()
+            t_us.append(t0_.elapsed_time(t1_) * 1e3)
+        tiled_bytes = 2 * resident * (pool_bytes + n_req_tok * w.num_kv_heads * w.head_dim * 2)
+        res["tiled_rebuild_us"] = round(float(np.median(t_us)), 1)
+        res["tiled_rebuild_GBps"] = round(tiled_bytes / (float(np.median(t_us)) * 1e-6) / 1e9, 2)
+        del tiled_src
     if args.ingress_requests and not mixed and not all_bf16:
         res["ingress"] = ingress_experiment(w, ctx, args.ingress_requests, attn_launch, resident,
                                             stream, max(args.steps, 10))

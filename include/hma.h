@@ -120,6 +120,47 @@ HMA_API int hma_bfp8_dequant_pages_naive(const uint8_t *src_mant, const uint8_t 
                                  void *stream);
 
 /*
+ * hma_bfp8_rebuild_tiled -- the rest of the decoder's single reconstruction
+ * pass (Sec. 3.3): the prefill side's tiled layout to row-major pages, the
+ * merge of the per-chip KV shards, and (keys) the post-rotary re-layout from
+ * interleaved pairs (2i, 2i+1) to half-split pairs (i, i + 64), together with
+ * the BFP8 -> BF16 decode.
+ *
+ * Source (the paper gives no tile byte order; this is the one fixed here):
+ * for each pool (a layer's K or V of one request), n_shards shards back to
+ * back; shard t (chip t) holds KV heads [t*Hs, (t+1)*Hs), Hs =
+ * num_kv_heads / n_shards, as 32x32-element tiles ordered [local head]
+ * [token tile: 32 tokens][channel tile: 32 channels], each tile 1088 bytes:
+ * 64 exponent bytes [face][row] then 1024 mantissa bytes [face][row][16];
+ * face f covers tile rows 16*(f/2).. and tile channels 16*(f%2)..; the 16
+ * channels of a face row (one token) share their exponent.  Rows past
+ * n_tokens in the last token tile are padding and are ignored.
+ *
+ * Output: token p of the request goes to slot p % 16 of page dst_pages[p / 16]
+ * of BF16 pool `pool`, KV head t*Hs + h, bit-exact.  With rope_reorder = 1,
+ * source channel c is written to channel c/2 (c even) or 64 + c/2 (c odd).
+ *
+ *   src        device bytes, 16-byte aligned; pool i at + i*src_pool_stride_bytes
+ *              (a multiple of 16, at least hma_tiled_shard_bytes() x n_shards)
+ *   dst_bf16   BF16 pool 0 [pages][Hkv][16][128], 16-byte aligned; pool i at
+ *              + i*dst_pool_stride_pages pages
+ *   dst_pages  int32 [ceil(n_tokens / 16)] device page ids, or NULL (page i)
+ *   num_kv_heads divisible by n_shards; head_dim 128, page_size 16
+ *   rope_reorder 0 (values, or keys already half-split) or 1 (keys)
+ * Errors: HMA_EINVAL, HMA_EUNSUPPORTED, HMA_EHIP.
+ */
+HMA_API int hma_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                           int32_t n_shards, int32_t n_tokens, uint16_t *dst_bf16,
+                           const int32_t *dst_pages, int64_t dst_pool_stride_pages,
+                           int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                           int32_t rope_reorder, void *stream);
+
+/* Bytes of one shard of hma_bfp8_rebuild_tiled's source (host only; -1 on
+ * invalid sizes): heads_per_shard x ceil(n_tokens / 32) x (head_dim / 32)
+ * tiles of 1088 bytes. */
+HMA_API int64_t hma_tiled_shard_bytes(int32_t n_tokens, int32_t heads_per_shard, int32_t head_dim);
+
+/*
  * hma_ingress_rebuild -- the decode-side end of the layer-wise transfer
  * pipeline (Sec. 3.2: the decoder overlaps receive, host-to-device copy and
  * dequantization with decode; Sec. 3.3: raw BFP8 bytes arrive verbatim and are

@@ -49,6 +49,10 @@ def lib() -> ctypes.CDLL:
     L.hma_bfp8_dequant_pages.restype = ctypes.c_int
     L.hma_bfp8_dequant_pages_naive.argtypes = L.hma_bfp8_dequant_pages.argtypes
     L.hma_bfp8_dequant_pages_naive.restype = ctypes.c_int
+    L.hma_bfp8_rebuild_tiled.argtypes = [vp, i64, i32, i32, i32, vp, vp, i64, i32, i32, i32, i32, vp]
+    L.hma_bfp8_rebuild_tiled.restype = ctypes.c_int
+    L.hma_tiled_shard_bytes.argtypes = [i32, i32, i32]
+    L.hma_tiled_shard_bytes.restype = i64
     L.hma_ingress_rebuild.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i64, i32, i32, i32, vp]
     L.hma_ingress_rebuild.restype = ctypes.c_int
     L.hma_decode_attn_bfp8.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, i32,
@@ -141,6 +145,31 @@ def bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pool
             page_size, _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_bfp8_dequant_pages" + ("_naive" if naive else ""))
+
+
+def tiled_shard_bytes(n_tokens: int, heads_per_shard: int, head_dim: int = HEAD_DIM) -> int:
+    """Bytes of one prefill shard in the tiled source layout."""
+    n = int(lib().hma_tiled_shard_bytes(n_tokens, heads_per_shard, head_dim))
+    if n < 0:
+        raise HmaError(HMA_EINVAL, "hma_tiled_shard_bytes")
+    return n
+
+
+def bfp8_rebuild_tiled(src, dst_bf16, n_tokens, n_shards, dst_pages=None, n_pools=1,
+                       src_pool_stride_bytes=0, dst_pool_stride_pages=0, rope_reorder=False,
+                       num_kv_heads=8, head_dim=HEAD_DIM, page_size=PAGE_SIZE, stream=None) -> None:
+    """hma_bfp8_rebuild_tiled: tiled per-chip prefill shards (uint8 device
+    tensor) -> BF16 pages of dst_bf16, with the rotary key re-layout when
+    rope_reorder is set."""
+    _check_dev(src, dst_bf16, dst_pages)
+    if dst_pages is not None and int(dst_pages.numel()) != (n_tokens + page_size - 1) // page_size:
+        raise ValueError("dst_pages must name one page per 16 tokens")
+    rc = lib().hma_bfp8_rebuild_tiled(_ptr(src), src_pool_stride_bytes, n_pools, n_shards, n_tokens,
+                                      _ptr(dst_bf16), _ptr(dst_pages), dst_pool_stride_pages,
+                                      num_kv_heads, head_dim, page_size, int(bool(rope_reorder)),
+                                      _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_bfp8_rebuild_tiled")
 
 
 def ingress_rebuild(host_mant, host_exp, stage_mant, stage_exp, dst_bf16, dst_pages=None,

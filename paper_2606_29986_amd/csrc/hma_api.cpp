@@ -202,6 +202,45 @@ int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8
     return rc == 0 ? HMA_OK : HMA_EHIP;
 }
 
+int64_t hma_tiled_shard_bytes(int32_t n_tokens, int32_t heads_per_shard, int32_t head_dim)
+{
+    if (n_tokens < 0 || heads_per_shard < 1 || head_dim != kSupportedHeadDim)
+        return -1;
+    return (int64_t)heads_per_shard * ((n_tokens + 31) / 32) * (head_dim / 32) * (64 + 32 * 32);
+}
+
+int hma_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                           int32_t n_shards, int32_t n_tokens, uint16_t *dst_bf16,
+                           const int32_t *dst_pages, int64_t dst_pool_stride_pages,
+                           int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                           int32_t rope_reorder, void *stream)
+{
+    if (n_pools < 0 || n_tokens < 0 || n_shards < 1 || num_kv_heads <= 0)
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (num_kv_heads % n_shards != 0 || (rope_reorder != 0 && rope_reorder != 1))
+        return HMA_EINVAL;
+    if (n_pools == 0 || n_tokens == 0)
+        return HMA_OK;
+    if (!src || !dst_bf16 || !aligned(src, 16) || !aligned(dst_bf16, 16))
+        return HMA_EINVAL;
+    const int64_t pool_bytes = (int64_t)n_shards * hma_tiled_shard_bytes(n_tokens, num_kv_heads / n_shards, head_dim);
+    if (n_pools > 1 && (src_pool_stride_bytes < pool_bytes || src_pool_stride_bytes % 16 != 0))
+        return HMA_EINVAL;
+    if (n_pools > 1 && dst_pool_stride_pages < 1)
+        return HMA_EINVAL;
+    if (dst_pool_stride_pages < 0 || src_pool_stride_bytes < 0)
+        return HMA_EINVAL;
+    const int64_t units = (int64_t)n_pools * num_kv_heads * ((n_tokens + 31) / 32);
+    if (units / 4 + 1 > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    const int rc = hma::launch_bfp8_rebuild_tiled(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens,
+                                                  dst_bf16, dst_pages, dst_pool_stride_pages, num_kv_heads,
+                                                  rope_reorder, static_cast<hipStream_t>(stream));
+    return rc == 0 ? HMA_OK : HMA_EHIP;
+}
+
 int32_t hma_decode_attn_tokens_per_split(int32_t batch, int32_t num_q_heads,
                                          int32_t num_kv_heads, int32_t max_context_len)
 {

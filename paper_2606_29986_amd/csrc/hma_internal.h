@@ -25,6 +25,12 @@ int launch_bfp8_dequant_pages_naive(const uint8_t *src_mant, const uint8_t *src_
                                     int32_t n_pages, int32_t n_pools, int64_t src_stride_pages,
                                     int64_t dst_stride_pages, int32_t hkv, hipStream_t stream);
 
+// Tiled per-chip prefill shards -> BF16 pages (see rebuild_tiled.hip).
+int launch_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                              int32_t n_shards, int32_t n_tokens, uint16_t *dst, const int32_t *dst_pages,
+                              int64_t dst_stride_pages, int32_t hkv, int32_t rope_reorder,
+                              hipStream_t stream);
+
 // Host -> device copy of the staged pages on `stream`, then their rebuild
 // (src = staged page i, dst = dst_pages[i] or i when NULL).
 int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,

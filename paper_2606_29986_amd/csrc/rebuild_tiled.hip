@@ -1,0 +1,108 @@
+// rebuild_tiled.hip -- tiled per-chip prefill shards -> BF16 pages (gfx950).
+//
+// The decoder's single reconstruction pass also converts the prefill side's
+// tiled layout to the row-major paged layout, merges the per-chip KV shards
+// and moves keys from the interleaved rotary order to the half-split order
+// (Sec. 3.3).  Tile byte order (the paper gives none; fixed here):
+//   shard t (chip t) holds KV heads [t*Hs, (t+1)*Hs);
+//   tiles [local head][token tile of 32][channel tile of 32], 1088 bytes each:
+//   64 exponent bytes [face][row], then 1024 mantissa bytes [face][row][16];
+//   face f covers tile rows 16*(f/2).. and tile channels 16*(f%2)..
+// With the rotary re-layout, source channel c goes to c/2 (even c) or
+// 64 + c/2 (odd c).
+//
+// One wave rebuilds one (pool, shard, local head, token tile): the four
+// channel tiles of a token tile are 4352 contiguous bytes, the output is 32
+// rows of 256 bytes (two page slots ranges).  The work is cut into 512 pieces
+// of 8 output channels (16 bytes): piece (row, q) writes output channels
+// [8q, 8q + 8) of tile row `row`; lane l takes pieces l + 64 s, s = 0..7, so
+// every store instruction writes 1 KB of consecutive page bytes.  A piece
+// reads the 8 source bytes it needs (half a face row), or with the rotary
+// re-layout the whole 16-byte face row whose even (q < 8) or odd (q >= 8)
+// channels it keeps.
+#include "hma_device.h"
+#include "hma_internal.h"
+
+namespace hma {
+
+constexpr int kTiledWaves = 4;
+constexpr int kTileBytes = 64 + 32 * 32;
+constexpr int kChanTiles = kHeadDim / 32;
+
+__global__ __launch_bounds__(64 * kTiledWaves) void bfp8_rebuild_tiled_kernel(
+    const uint8_t *__restrict__ src, int64_t src_pool_stride_bytes, int64_t shard_bytes,
+    int32_t n_shards, int32_t heads_per_shard, int32_t token_tiles, int32_t n_tokens, int64_t n_units,
+    uint16_t *__restrict__ dst, const int32_t *__restrict__ dst_pages, int64_t dst_stride_pages,
+    int32_t hkv, int32_t rope_reorder)
+{
+    const int64_t unit = (int64_t)blockIdx.x * kTiledWaves + (threadIdx.x >> 6);
+    if (unit >= n_units)
+        return;
+    const int lane = threadIdx.x & 63;
+    const int tt = (int)(unit % token_tiles);
+    int64_t rest = unit / token_tiles;
+    const int h = (int)(rest % heads_per_shard);
+    rest /= heads_per_shard;
+    const int t = (int)(rest % n_shards);
+    const int64_t pool = rest / n_shards;
+    const uint8_t *tiles = src + pool * src_pool_stride_bytes + t * shard_bytes
+                           + ((int64_t)h * token_tiles + tt) * kChanTiles * kTileBytes;
+    const int q = lane & 15;                       // output channels [8q, 8q + 8)
+    // source face row of this piece: channels [16 c16, 16 c16 + 16) of the row
+    const int c16 = rope_reorder ? (q & 7) : (q >> 1);
+    const uint8_t *tile = tiles + (c16 >> 1) * kTileBytes;
+    const int fc = c16 & 1;
+
+    uint32_t w0[8], w1[8], ex[8];
+#pragma unroll
+    for (int s = 0; s < 8; s++) {
+        const int r = 4 * s + (lane >> 4);       // tile row
+        const int face = 2 * (r >> 4) + fc;
+        const uint8_t *frow = tile + 64 + face * 256 + (r & 15) * 16;
+        ex[s] = tile[face * 16 + (r & 15)];
+        if (rope_reorder) {
+            // keep the even (q < 8) or odd (q >= 8) bytes of the face row
+            const u32x4_t v = *reinterpret_cast<const u32x4_t *>(frow);
+            const uint32_t sel = q < 8 ? 0x06040200u : 0x07050301u;
+            w0[s] = __builtin_amdgcn_perm(v.y, v.x, sel);
+            w1[s] = __builtin_amdgcn_perm(v.w, v.z, sel);
+        } else {
+            const u32x2_t v = *reinterpret_cast<const u32x2_t *>(frow + 8 * (q & 1));
+            w0[s] = v.x;
+            w1[s] = v.y;
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < 8; s++) {
+        const int r = 4 * s + (lane >> 4);
+        const int token = 32 * tt + r;
+        if (token < n_tokens) {
+            const int es = (int)ex[s] - kExpBias;
+            const u32x2_t a = bfp8_word_to_bf16(w0[s], es);
+            const u32x2_t c = bfp8_word_to_bf16(w1[s], es);
+            const int32_t pidx = token / kPageSize;
+            const int64_t page = pool * dst_stride_pages + (dst_pages ? dst_pages[pidx] : pidx);
+            uint16_t *out = dst + ((page * hkv + (int64_t)t * heads_per_shard + h) * kPageSize
+                                   + token % kPageSize) * kHeadDim + 8 * q;
+            __builtin_nontemporal_store(u32x4_t{a.x, a.y, c.x, c.y}, reinterpret_cast<u32x4_t *>(out));
+        }
+    }
+}
+
+int launch_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                              int32_t n_shards, int32_t n_tokens, uint16_t *dst, const int32_t *dst_pages,
+                              int64_t dst_stride_pages, int32_t hkv, int32_t rope_reorder,
+                              hipStream_t stream)
+{
+    const int32_t hs = hkv / n_shards;
+    const int32_t token_tiles = (n_tokens + 31) / 32;
+    const int64_t shard_bytes = (int64_t)hs * token_tiles * kChanTiles * kTileBytes;
+    const int64_t n_units = (int64_t)n_pools * n_shards * hs * token_tiles;
+    const int64_t blocks = (n_units + kTiledWaves - 1) / kTiledWaves;
+    hipLaunchKernelGGL(bfp8_rebuild_tiled_kernel, dim3((unsigned)blocks), dim3(64 * kTiledWaves), 0, stream,
+                       src, src_pool_stride_bytes, shard_bytes, n_shards, hs, token_tiles, n_tokens, n_units,
+                       dst, dst_pages, dst_stride_pages, hkv, rope_reorder);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+}  // namespace hma

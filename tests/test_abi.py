@@ -26,6 +26,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["hma_bfp8_dequant_pages", "hma_bfp8_dequant_pages_naive",
+                            "hma_bfp8_rebuild_tiled", "hma_tiled_shard_bytes",
                             "hma_decode_attn_bfp8",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
                             "hma_ingress_rebuild", "hma_status_string"])
@@ -126,6 +127,42 @@ def test_ingress_validation():
     assert _ingress(dst_stride=0) == hma.HMA_EINVAL          # two pools need a stride
     assert _ingress(se=FAKE * 2 + 64) == hma.HMA_EINVAL      # staging buffers overlap
     assert _ingress(dst=FAKE * 2) == hma.HMA_EINVAL          # destination is the staging
+
+
+def test_tiled_shard_bytes_matches_the_oracle():
+    import oracle
+    for n, hs in ((1, 1), (31, 2), (32, 2), (33, 8), (8192, 2)):
+        assert hma.tiled_shard_bytes(n, hs) == oracle.tiled_shard_bytes(n, hs)
+    with pytest.raises(hma.HmaError):
+        hma.tiled_shard_bytes(-1, 2)
+    with pytest.raises(hma.HmaError):
+        hma.tiled_shard_bytes(32, 2, head_dim=64)
+
+
+def _tiled(**kw):
+    a = dict(src=FAKE, stride=0, pools=1, shards=4, n=100, dst=FAKE * 2, pages=None, dstride=0,
+             hkv=8, D=128, P=16, rope=1)
+    a.update(kw)
+    return hma.lib().hma_bfp8_rebuild_tiled(a["src"], a["stride"], a["pools"], a["shards"], a["n"],
+                                            a["dst"], a["pages"], a["dstride"], a["hkv"], a["D"],
+                                            a["P"], a["rope"], None)
+
+
+def test_tiled_rebuild_validation():
+    assert _tiled(n=0) == hma.HMA_OK
+    assert _tiled(pools=0) == hma.HMA_OK
+    assert _tiled(n=-1) == hma.HMA_EINVAL
+    assert _tiled(shards=0) == hma.HMA_EINVAL
+    assert _tiled(shards=3) == hma.HMA_EINVAL            # 8 heads over 3 chips
+    assert _tiled(rope=2) == hma.HMA_EINVAL
+    assert _tiled(D=64) == hma.HMA_EUNSUPPORTED
+    assert _tiled(src=None) == hma.HMA_EINVAL
+    assert _tiled(dst=None) == hma.HMA_EINVAL
+    assert _tiled(src=MISALIGNED) == hma.HMA_EINVAL
+    assert _tiled(pools=2, stride=64, dstride=10) == hma.HMA_EINVAL      # pools overlap
+    need = 4 * hma.tiled_shard_bytes(100, 2)
+    assert _tiled(pools=2, stride=need + 8, dstride=10) == hma.HMA_EINVAL  # stride not 16-aligned
+    assert _tiled(pools=2, stride=need, dstride=0) == hma.HMA_EINVAL
 
 
 def _attn(**kw):
