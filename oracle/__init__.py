@@ -84,10 +84,13 @@ def lib():
         L.ora_rebuild_tiled.argtypes = [_p(u8), i64, i32, i32, i32, i32, i32, i32, i32, _p(u16),
                                         _p(i32), i64]
         L.ora_rebuild_tiled.restype = None
+        L.ora_pack_tiled.argtypes = [_p(u8), i64, i32, i32, i32, i32, i32, i32, _p(u8), _p(u8),
+                                     _p(i32), i64]
+        L.ora_pack_tiled.restype = None
         L.ora_merge_partials.argtypes = [i32, _p(f64), _p(f64), _p(f64), i32, _p(f64), _p(f64)]
         L.ora_merge_partials.restype = None
         L.ora_decode_attn.argtypes = [_p(u16), _p(u8), _p(u8), _p(u8), _p(u8), _p(u16), _p(u16),
-                                      _p(i32), i32, _p(i32), i32, i32, i32, i32, i32, f64,
+                                      _p(i32), i32, _p(i32), i32, i32, i32, i32, i32, f64, i32,
                                       _p(f64), _p(f64)]
         L.ora_decode_attn.restype = ctypes.c_int
         L.ora_decode_attn_split_one.argtypes = [_p(u16), _p(u8), _p(u8), _p(u8), _p(u8), _p(u16),
@@ -211,16 +214,32 @@ def rebuild_tiled(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens, num_k
     return dst
 
 
+def pack_tiled(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens, num_kv_heads, dst_mant,
+               dst_exp, dst_pages, dst_pool_stride_pages, head_dim=128, page_size=16):
+    """Tiled shards -> BFP8 pages, bytes unchanged (dst_* modified in place)."""
+    assert dst_mant.dtype == np.uint8 and dst_exp.dtype == np.uint8
+    assert dst_mant.flags["C_CONTIGUOUS"] and dst_exp.flags["C_CONTIGUOUS"]
+    s = _c(src, np.uint8)
+    dp = _c(dst_pages, np.int32)
+    lib().ora_pack_tiled(_ptr(s, ctypes.c_uint8), src_pool_stride_bytes, n_pools, n_shards,
+                         n_tokens, num_kv_heads, head_dim, page_size,
+                         _ptr(dst_mant, ctypes.c_uint8), _ptr(dst_exp, ctypes.c_uint8),
+                         _ptr(dp, ctypes.c_int32), dst_pool_stride_pages)
+    return dst_mant, dst_exp
+
+
 # ---------------------------------------------------------- attention
 
 def decode_attn(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, context_lens,
-                num_kv_heads, page_size, scale):
+                num_kv_heads, page_size, scale, key_order=0):
     """float64 paged decode attention.
 
     q: uint16 [B][Hq][D] BF16 bits.  Pools as in the library (flat or shaped).
     page_table: int32 [B][max_pages]; context_lens: int32 [B].
     scale: float; it is first rounded to float32 (the library takes a float)
     and then widened, so both sides use the same scale value.
+    key_order=1: K rows are stored in the interleaved rotary order and are
+    relabelled to the queries' half-split order on read.
     Returns (out float64 [B][Hq][D], lse float64 [B][Hq])."""
     q = _c(q, np.uint16)
     B, Hq, D = q.shape
@@ -237,7 +256,7 @@ def decode_attn(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, con
         _ptr(arrs[2], ctypes.c_uint8), _ptr(arrs[3], ctypes.c_uint8),
         _ptr(arrs[4], ctypes.c_uint16), _ptr(arrs[5], ctypes.c_uint16),
         _ptr(pt, ctypes.c_int32), pt.shape[1], _ptr(cl, ctypes.c_int32),
-        B, Hq, num_kv_heads, D, page_size, float(np.float32(scale)),
+        B, Hq, num_kv_heads, D, page_size, float(np.float32(scale)), int(key_order),
         _ptr(out, ctypes.c_double), _ptr(lse, ctypes.c_double))
     if rc != 0:
         raise ValueError("oracle decode_attn: bad arguments")

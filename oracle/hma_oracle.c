@@ -268,6 +268,41 @@ void ora_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_
                     }
 }
 
+/* Tiled shards -> BFP8 pages, bytes unchanged: the layout half of the pass
+ * above, for a decoder that keeps the raw BFP8 pages and decodes them inside
+ * attention [Sec. 3.3].  Keys keep the interleaved rotary order (a 16-channel
+ * block cannot be relabelled without re-encoding); attention accounts for it
+ * (key_order).  Token p goes to slot p % P of page dst_pages[p / P] of pool
+ * `pool` (mantissa pool [pages][Hkv][P][D], exponent pool [pages][Hkv][P][D/16]). */
+void ora_pack_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                    int32_t n_shards, int32_t n_tokens, int32_t num_kv_heads, int32_t head_dim,
+                    int32_t page_size, uint8_t *dst_mant, uint8_t *dst_exp,
+                    const int32_t *dst_pages, int64_t dst_pool_stride_pages)
+{
+    const int32_t hs = num_kv_heads / n_shards;
+    const int32_t token_tiles = (n_tokens + 31) / 32;
+    const int32_t chan_tiles = head_dim / 32;
+    const int64_t tile_bytes = 64 + 32 * 32;
+    const int64_t shard_bytes = (int64_t)hs * token_tiles * chan_tiles * tile_bytes;
+    for (int32_t pool = 0; pool < n_pools; pool++)
+        for (int32_t t = 0; t < n_shards; t++)
+            for (int32_t h = 0; h < hs; h++)
+                for (int32_t p = 0; p < n_tokens; p++) {
+                    const int64_t page = pool * dst_pool_stride_pages + dst_pages[p / page_size];
+                    const int64_t row = (page * num_kv_heads + (int64_t)t * hs + h) * page_size + p % page_size;
+                    for (int32_t c = 0; c < head_dim; c++) {
+                        const int64_t tile_index = ((int64_t)h * token_tiles + p / 32) * chan_tiles + c / 32;
+                        const uint8_t *tile = src + pool * src_pool_stride_bytes + t * shard_bytes
+                                              + tile_index * tile_bytes;
+                        const int rr = p % 32, cc = c % 32;
+                        const int face = (rr / 16) * 2 + cc / 16;
+                        dst_mant[row * head_dim + c] = tile[64 + face * 256 + (rr % 16) * 16 + cc % 16];
+                        if (c % ORA_BLOCK == 0)
+                            dst_exp[row * (head_dim / ORA_BLOCK) + c / ORA_BLOCK] = tile[face * 16 + rr % 16];
+                    }
+                }
+}
+
 /* ----------------------------------------------------- paged attention */
 
 typedef struct {
@@ -275,12 +310,33 @@ typedef struct {
     const uint16_t *k_bf16, *v_bf16;
     const int32_t *page_table;
     int32_t max_pages_per_seq, num_kv_heads, head_dim, page_size;
+    int32_t key_order;   /* 1: K rows stored in the interleaved rotary order */
 } ora_kv;
 
 /* Gather one K or V row of logical token t of sequence b, kv head j, into
  * row[head_dim] as float64 [Sec. 3.3: BFP8 pages decoded on read, BF16 pages
- * read as stored]. */
+ * read as stored].  With key_order set, K rows are stored as the prefill side
+ * leaves them (rotary pairs (2i, 2i+1)) and are relabelled into the
+ * half-split order of the queries (pairs (i, i + D/2)) [Sec. 3.3: post-RoPE
+ * key re-layout]: stored channel 2i is key channel i, 2i+1 is D/2 + i. */
+static void ora_gather_row_stored(const ora_kv *kv, int is_v, int b, int j, int t, double *row);
+
 static void ora_gather_row(const ora_kv *kv, int is_v, int b, int j, int t, double *row)
+{
+    if (is_v || !kv->key_order) {
+        ora_gather_row_stored(kv, is_v, b, j, t, row);
+        return;
+    }
+    const int D = kv->head_dim;
+    double stored[D];
+    ora_gather_row_stored(kv, is_v, b, j, t, stored);
+    for (int i = 0; i < D / 2; i++) {
+        row[i] = stored[2 * i];
+        row[D / 2 + i] = stored[2 * i + 1];
+    }
+}
+
+static void ora_gather_row_stored(const ora_kv *kv, int is_v, int b, int j, int t, double *row)
 {
     int32_t entry = kv->page_table[(int64_t)b * kv->max_pages_per_seq + t / kv->page_size];
     int slot = t % kv->page_size;
@@ -384,12 +440,12 @@ int ora_decode_attn(const uint16_t *q,
                     const uint16_t *k_bf16, const uint16_t *v_bf16,
                     const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *context_lens,
                     int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim,
-                    int32_t page_size, double scale, double *out, double *lse)
+                    int32_t page_size, double scale, int32_t key_order, double *out, double *lse)
 {
     if (num_kv_heads <= 0 || num_q_heads % num_kv_heads != 0 || head_dim % ORA_BLOCK != 0)
         return -1;
     ora_kv kv = {k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table,
-                 max_pages_per_seq, num_kv_heads, head_dim, page_size};
+                 max_pages_per_seq, num_kv_heads, head_dim, page_size, key_order};
     const int g = num_q_heads / num_kv_heads;
     int max_ctx = 0;
     for (int b = 0; b < batch; b++)
@@ -440,7 +496,7 @@ int ora_decode_attn_split_one(const uint16_t *q,
         if (bounds[s + 1] < bounds[s])
             return -1;
     ora_kv kv = {k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table,
-                 max_pages_per_seq, num_kv_heads, head_dim, page_size};
+                 max_pages_per_seq, num_kv_heads, head_dim, page_size, 0};
     const int g = num_q_heads / num_kv_heads;
     int ctx = context_lens[b];
     double *scores = (double *)malloc(sizeof(double) * (size_t)(ctx > 0 ? ctx : 1));

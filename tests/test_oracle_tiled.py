@@ -16,6 +16,7 @@ import numpy as np
 import pytest
 
 import oracle
+import workloads as wl
 
 D, P = 128, 16
 
@@ -127,3 +128,76 @@ def test_key_relayout_is_the_rotary_relabelling():
         lhs = _rotate(x, inter, pos * theta_base)[perm]      # rotate on the prefill side, relabel
         rhs = _rotate(x[perm], half, pos * theta_base)       # relabel, rotate the decode-side way
         np.testing.assert_allclose(lhs, rhs, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n_shards,n_tokens", [(1, 5), (2, 47), (4, 200), (8, 33)])
+def test_pack_keeps_the_bytes_of_row_major_pages(n_shards, n_tokens):
+    """Packing tiled shards back into BFP8 pages returns the page bytes that
+    the numpy re-tiling started from (slots past the last token untouched)."""
+    rng = np.random.default_rng(300 + n_tokens)
+    hkv, pool_pages = 8, 30
+    n_req = (n_tokens + P - 1) // P
+    mant, ex = _pages(rng, pool_pages, hkv)
+    src_list = rng.choice(pool_pages, n_req, replace=False)
+    shards = _shards_from_pages(mant, ex, src_list, n_tokens, n_shards, rng)
+    dst_pages = rng.choice(pool_pages, n_req, replace=False).astype(np.int32)
+    pm = np.full((pool_pages, hkv, P, D), 0xA5, np.uint8)
+    pe = np.full((pool_pages, hkv, P, D // 16), 0xA5, np.uint8)
+    oracle.pack_tiled(shards, 0, 1, n_shards, n_tokens, hkv, pm, pe, dst_pages, 0)
+    for p in range(n_tokens):
+        assert np.array_equal(pm[dst_pages[p // P], :, p % P], mant[src_list[p // P], :, p % P])
+        assert np.array_equal(pe[dst_pages[p // P], :, p % P], ex[src_list[p // P], :, p % P])
+    if n_tokens % P:
+        assert (pm[dst_pages[-1], :, n_tokens % P:] == 0xA5).all()
+
+
+def _relayout_perm():
+    """Output position -> source channel of the oracle's key re-layout (the
+    permutation pinned by the rotary identity above)."""
+    tiles = np.zeros(oracle.tiled_shard_bytes(1, 1), np.uint8).reshape(D // 32, 1088)
+    for ct in range(D // 32):
+        tiles[ct, :64] = 133
+        for cc in range(32):
+            tiles[ct, 64 + (cc // 16) * 256 + cc % 16] = 32 * ct + cc
+    out = np.zeros((1, 1, P, D), np.uint16)
+    oracle.rebuild_tiled(tiles.reshape(-1), 0, 1, 1, 1, 1, out, np.zeros(1, np.int32), 0, True)
+    return oracle.bf16_to_f64(out[0, 0, 0]).astype(int)
+
+
+def test_attention_over_interleaved_keys_matches_sdpa_on_relabelled_keys():
+    """key_order = 1: K pages hold the rows as the prefill side leaves them.
+    The result must equal float64 attention (torch SDPA) over the keys
+    relabelled with the re-layout permutation, and attention over BF16 pages
+    that already hold the relabelled keys."""
+    import torch
+    rng = np.random.default_rng(9)
+    B, Hq, hkv, ctx = 2, 8, 2, 45
+    n_pages = 2 * ((ctx + P - 1) // P)
+    k_mant, k_exp = _pages(rng, n_pages, hkv)
+    k_exp[:] = rng.integers(120, 134, k_exp.shape, dtype=np.uint8)
+    v_mant, v_exp = _pages(rng, n_pages, hkv)
+    v_exp[:] = rng.integers(120, 134, v_exp.shape, dtype=np.uint8)
+    pt = np.arange(n_pages, dtype=np.int32).reshape(B, -1)
+    cl = np.full(B, ctx, np.int32)
+    q = wl.f32_to_bf16_bits(rng.standard_normal((B, Hq, D)).astype(np.float32))
+    scale = 1.0 / np.sqrt(D)
+    out, lse = oracle.decode_attn(q, k_mant, k_exp, v_mant, v_exp, None, None, pt, cl, hkv, P, scale,
+                                  key_order=1)
+    perm = _relayout_perm()
+    kd = oracle.bf16_to_f64(oracle.decode_blocks(k_mant, k_exp))[..., perm]   # relabelled keys
+    vd = oracle.bf16_to_f64(oracle.decode_blocks(v_mant, v_exp))
+    s32 = float(np.float32(scale))
+    for b in range(B):
+        K = np.concatenate([kd[pt[b, i]] for i in range(pt.shape[1])], axis=1)[:, :ctx]  # [hkv][t][D]
+        V = np.concatenate([vd[pt[b, i]] for i in range(pt.shape[1])], axis=1)[:, :ctx]
+        qf = torch.from_numpy(oracle.bf16_to_f64(q[b])).view(hkv, Hq // hkv, 1, D)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            qf, torch.from_numpy(K)[:, None], torch.from_numpy(V)[:, None], scale=s32)
+        np.testing.assert_allclose(out[b], ref.reshape(Hq, D).numpy(), rtol=0, atol=1e-12)
+    # the same keys as BF16 pages already in half-split order, read without relabelling
+    kb = oracle.decode_blocks(k_mant, k_exp)[..., perm].copy()
+    vb = oracle.decode_blocks(v_mant, v_exp)
+    out2, lse2 = oracle.decode_attn(q, k_mant, k_exp, v_mant, v_exp, kb, vb, pt | 0x40000000, cl,
+                                    hkv, P, scale)
+    np.testing.assert_allclose(out, out2, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, lse2, rtol=0, atol=1e-12)
