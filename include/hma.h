@@ -155,6 +155,24 @@ HMA_API int hma_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_b
                            int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
                            int32_t rope_reorder, void *stream);
 
+/*
+ * hma_bfp8_pack_tiled -- the layout half of the same pass for a decoder that
+ * keeps raw BFP8 pages (Sec. 3.3): the tiled shards (source exactly as for
+ * hma_bfp8_rebuild_tiled) become BFP8 pages -- mantissa rows of 128 bytes and
+ * exponent rows of 8 -- with every byte unchanged and the shards merged.
+ * Keys keep the interleaved rotary order (a 16-channel block cannot be
+ * relabelled without re-encoding): read them with hma_decode_attn_bfp8's
+ * key_order = 1.
+ *   dst_mant  uint8 mantissa pool 0 [pages][Hkv][16][128], 16-byte aligned
+ *   dst_exp   uint8 exponent pool 0 [pages][Hkv][16][8], 16-byte aligned
+ *   pool i at + i*dst_pool_stride_pages pages of both; other arguments and
+ *   errors as hma_bfp8_rebuild_tiled.
+ */
+HMA_API int hma_bfp8_pack_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                        int32_t n_shards, int32_t n_tokens, uint8_t *dst_mant, uint8_t *dst_exp,
+                        const int32_t *dst_pages, int64_t dst_pool_stride_pages, int32_t num_kv_heads,
+                        int32_t head_dim, int32_t page_size, void *stream);
+
 /* Bytes of one shard of hma_bfp8_rebuild_tiled's source (host only; -1 on
  * invalid sizes): heads_per_shard x ceil(n_tokens / 32) x (head_dim / 32)
  * tiles of 1088 bytes. */
@@ -222,6 +240,12 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *   num_q_heads % num_kv_heads == 0 and num_q_heads / num_kv_heads <= 16;
  *   head_dim == 128, page_size == 16
  *   scale      softmax scale (typically 1/sqrt(128))
+ *   key_order  0: K pages hold key channels in the queries' order (half-split
+ *              rotary pairs (i, i + 64)); 1: K pages (of both formats) hold
+ *              them as the prefill side leaves them, rotary pairs (2i, 2i+1):
+ *              stored channel 2i is key channel i and 2i+1 is 64 + i (the
+ *              paper's post-RoPE key re-layout, Sec. 3.3, absorbed by
+ *              permuting the query once instead of the keys)
  *   tokens_per_split  0 = chosen by the library (see
  *              hma_decode_attn_tokens_per_split); else a positive multiple
  *              of page_size (16), at most 16384
@@ -240,6 +264,7 @@ HMA_API int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const
                          int32_t max_pages_per_seq, const int32_t *context_lens,
                          int32_t max_context_len, int32_t batch, int32_t num_q_heads,
                          int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
+                         int32_t key_order,
                          int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
                          size_t workspace_bytes, void *stream);
 

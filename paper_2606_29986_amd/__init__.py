@@ -51,12 +51,15 @@ def lib() -> ctypes.CDLL:
     L.hma_bfp8_dequant_pages_naive.restype = ctypes.c_int
     L.hma_bfp8_rebuild_tiled.argtypes = [vp, i64, i32, i32, i32, vp, vp, i64, i32, i32, i32, i32, vp]
     L.hma_bfp8_rebuild_tiled.restype = ctypes.c_int
+    L.hma_bfp8_pack_tiled.argtypes = [vp, i64, i32, i32, i32, vp, vp, vp, i64, i32, i32, i32, vp]
+    L.hma_bfp8_pack_tiled.restype = ctypes.c_int
     L.hma_tiled_shard_bytes.argtypes = [i32, i32, i32]
     L.hma_tiled_shard_bytes.restype = i64
     L.hma_ingress_rebuild.argtypes = [vp, vp, vp, vp, vp, vp, i32, i32, i64, i32, i32, i32, vp]
     L.hma_ingress_rebuild.restype = ctypes.c_int
     L.hma_decode_attn_bfp8.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, i32,
-                                       i32, i32, i32, ctypes.c_float, i32, vp, vp, vp, sz, vp]
+                                       i32, i32, i32, ctypes.c_float, i32, i32, vp, vp, vp, sz,
+                                       vp]
     L.hma_decode_attn_bfp8.restype = ctypes.c_int
     L.hma_decode_attn_tokens_per_split.argtypes = [i32, i32, i32, i32]
     L.hma_decode_attn_tokens_per_split.restype = i32
@@ -172,6 +175,22 @@ def bfp8_rebuild_tiled(src, dst_bf16, n_tokens, n_shards, dst_pages=None, n_pool
         raise HmaError(rc, "hma_bfp8_rebuild_tiled")
 
 
+def bfp8_pack_tiled(src, dst_mant, dst_exp, n_tokens, n_shards, dst_pages=None, n_pools=1,
+                    src_pool_stride_bytes=0, dst_pool_stride_pages=0, num_kv_heads=8,
+                    head_dim=HEAD_DIM, page_size=PAGE_SIZE, stream=None) -> None:
+    """hma_bfp8_pack_tiled: tiled per-chip prefill shards -> BFP8 pages,
+    bytes unchanged (keys stay in the interleaved rotary order)."""
+    _check_dev(src, dst_mant, dst_exp, dst_pages)
+    if dst_pages is not None and int(dst_pages.numel()) != (n_tokens + page_size - 1) // page_size:
+        raise ValueError("dst_pages must name one page per 16 tokens")
+    rc = lib().hma_bfp8_pack_tiled(_ptr(src), src_pool_stride_bytes, n_pools, n_shards, n_tokens,
+                                   _ptr(dst_mant), _ptr(dst_exp), _ptr(dst_pages),
+                                   dst_pool_stride_pages, num_kv_heads, head_dim, page_size,
+                                   _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_bfp8_pack_tiled")
+
+
 def ingress_rebuild(host_mant, host_exp, stage_mant, stage_exp, dst_bf16, dst_pages=None,
                     n_pools=1, dst_pool_stride_pages=0, num_kv_heads=8, head_dim=HEAD_DIM,
                     page_size=PAGE_SIZE, stream=None) -> None:
@@ -204,12 +223,13 @@ def ingress_rebuild(host_mant, host_exp, stage_mant, stage_exp, dst_bf16, dst_pa
 def decode_attn_bfp8(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len,
                      out, k_bf16=None, v_bf16=None, lse=None, scale=None, num_kv_heads=None,
                      tokens_per_split=0, workspace=None, head_dim=HEAD_DIM, page_size=PAGE_SIZE,
-                     stream=None) -> None:
+                     key_order=0, stream=None) -> None:
     """hma_decode_attn_bfp8: fused BFP8 paged decode attention into ``out``.
 
     q, out: [B][Hq][128] 16-bit tensors (BF16 bits); pools as in hma.h;
     page_table int32 [B][max_pages]; context_lens int32 [B];
-    max_context_len: host int bound.  num_kv_heads defaults to k_mant.shape[1]."""
+    max_context_len: host int bound.  num_kv_heads defaults to k_mant.shape[1].
+    key_order=1: K pages hold channels in the interleaved rotary order."""
     _check_dev(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, out, k_bf16, v_bf16,
                lse, workspace)
     B, Hq, D = q.shape
@@ -220,7 +240,8 @@ def decode_attn_bfp8(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, 
     rc = lib().hma_decode_attn_bfp8(
         _ptr(q), _ptr(k_mant), _ptr(k_exp), _ptr(v_mant), _ptr(v_exp), _ptr(k_bf16),
         _ptr(v_bf16), _ptr(page_table), int(page_table.shape[1]), _ptr(context_lens),
-        int(max_context_len), B, Hq, hkv, D, page_size, float(scale), int(tokens_per_split),
+        int(max_context_len), B, Hq, hkv, D, page_size, float(scale), int(key_order),
+        int(tokens_per_split),
         _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_decode_attn_bfp8")

@@ -68,6 +68,7 @@ struct AttnParams {
     float2 *part_ml;
     float *part_o;
     int32_t max_pages, batch, hq, hkv, g, tps, n_splits;
+    int32_t key_interleaved;
     float scale_log2;
 };
 
@@ -583,13 +584,25 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
             sm_pt[i] = (uint32_t)pt[i];
     }
 
-    // Q^T operand (column r = head j*g + r; zero for padded heads)
+    // Q^T operand (column r = head j*g + r; zero for padded heads).  Keys kept
+    // in the interleaved rotary order (stored channel 2i = key channel i,
+    // 2i + 1 = 64 + i) are met by permuting q the same way once, here:
+    // stored channels c0..c0+7 take q[c0/2 ..] and q[64 + c0/2 ..] in turn.
     u32x4_t qB[4];
     {
         const uint16_t *qrow = p.q + out_row * kHeadDim;
 #pragma unroll
         for (int kk = 0; kk < 4; kk++) {
-            u32x4_t v = *reinterpret_cast<const u32x4_t *>(qrow + qk_channel(G, kk));
+            const int c0 = qk_channel(G, kk);
+            u32x4_t v;
+            if (p.key_interleaved) {
+                const u32x2_t a = *reinterpret_cast<const u32x2_t *>(qrow + c0 / 2);
+                const u32x2_t b = *reinterpret_cast<const u32x2_t *>(qrow + kHeadDim / 2 + c0 / 2);
+                v = u32x4_t{__builtin_amdgcn_perm(b.x, a.x, kPermLoHalves), __builtin_amdgcn_perm(b.x, a.x, kPermHiHalves),
+                            __builtin_amdgcn_perm(b.y, a.y, kPermLoHalves), __builtin_amdgcn_perm(b.y, a.y, kPermHiHalves)};
+            } else {
+                v = *reinterpret_cast<const u32x4_t *>(qrow + c0);
+            }
             qB[kk] = head_ok ? v : u32x4_t{0u, 0u, 0u, 0u};
         }
     }
@@ -804,6 +817,7 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
     p.g = a.hq / a.hkv;
     p.tps = a.tps;
     p.n_splits = a.n_splits;
+    p.key_interleaved = a.key_interleaved;
     p.scale_log2 = a.scale * kLog2e;
     p.tickets = nullptr;
     p.part_ml = nullptr;

@@ -117,6 +117,40 @@ int dequant_checked(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *d
     return rc == 0 ? HMA_OK : HMA_EHIP;
 }
 
+int64_t tiled_shard_bytes(int32_t n_tokens, int32_t heads_per_shard)
+{
+    return (int64_t)heads_per_shard * ((n_tokens + 31) / 32) * (kSupportedHeadDim / 32) * (64 + 32 * 32);
+}
+
+// Shared argument checks of the tiled-source entry points (HMA_OK also when
+// there is nothing to do: the caller then returns without launching).
+int tiled_check(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools, int32_t n_shards,
+                int32_t n_tokens, const void *dst_a, const void *dst_b, int64_t dst_pool_stride_pages,
+                int32_t num_kv_heads, int32_t head_dim, int32_t page_size)
+{
+    if (n_pools < 0 || n_tokens < 0 || n_shards < 1 || num_kv_heads <= 0)
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (num_kv_heads % n_shards != 0)
+        return HMA_EINVAL;
+    if (n_pools == 0 || n_tokens == 0)
+        return HMA_OK;
+    if (!src || !dst_a || !dst_b || !aligned(src, 16) || !aligned(dst_a, 16) || !aligned(dst_b, 16))
+        return HMA_EINVAL;
+    const int64_t pool_bytes = (int64_t)n_shards * tiled_shard_bytes(n_tokens, num_kv_heads / n_shards);
+    if (n_pools > 1 && (src_pool_stride_bytes < pool_bytes || src_pool_stride_bytes % 16 != 0))
+        return HMA_EINVAL;
+    if (n_pools > 1 && dst_pool_stride_pages < 1)
+        return HMA_EINVAL;
+    if (dst_pool_stride_pages < 0 || src_pool_stride_bytes < 0)
+        return HMA_EINVAL;
+    const int64_t units = (int64_t)n_pools * num_kv_heads * ((n_tokens + 31) / 32);
+    if (units / 4 + 1 > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    return HMA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -134,7 +168,7 @@ const char *hma_status_string(int status)
     case HMA_EWORKSPACE:
         return "workspace missing or too small";
     case HMA_EHIP:
-        return "HIP kernel launch failed";
+        return "HIP launch or copy failed";
     default:
         return "unknown status";
     }
@@ -206,7 +240,7 @@ int64_t hma_tiled_shard_bytes(int32_t n_tokens, int32_t heads_per_shard, int32_t
 {
     if (n_tokens < 0 || heads_per_shard < 1 || head_dim != kSupportedHeadDim)
         return -1;
-    return (int64_t)heads_per_shard * ((n_tokens + 31) / 32) * (head_dim / 32) * (64 + 32 * 32);
+    return tiled_shard_bytes(n_tokens, heads_per_shard);
 }
 
 int hma_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
@@ -215,29 +249,32 @@ int hma_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, in
                            int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
                            int32_t rope_reorder, void *stream)
 {
-    if (n_pools < 0 || n_tokens < 0 || n_shards < 1 || num_kv_heads <= 0)
+    if (rope_reorder != 0 && rope_reorder != 1)
         return HMA_EINVAL;
-    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
-        return HMA_EUNSUPPORTED;
-    if (num_kv_heads % n_shards != 0 || (rope_reorder != 0 && rope_reorder != 1))
-        return HMA_EINVAL;
-    if (n_pools == 0 || n_tokens == 0)
-        return HMA_OK;
-    if (!src || !dst_bf16 || !aligned(src, 16) || !aligned(dst_bf16, 16))
-        return HMA_EINVAL;
-    const int64_t pool_bytes = (int64_t)n_shards * hma_tiled_shard_bytes(n_tokens, num_kv_heads / n_shards, head_dim);
-    if (n_pools > 1 && (src_pool_stride_bytes < pool_bytes || src_pool_stride_bytes % 16 != 0))
-        return HMA_EINVAL;
-    if (n_pools > 1 && dst_pool_stride_pages < 1)
-        return HMA_EINVAL;
-    if (dst_pool_stride_pages < 0 || src_pool_stride_bytes < 0)
-        return HMA_EINVAL;
-    const int64_t units = (int64_t)n_pools * num_kv_heads * ((n_tokens + 31) / 32);
-    if (units / 4 + 1 > (int64_t)INT_MAX)
-        return HMA_EINVAL;
+    const int st = tiled_check(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens, dst_bf16, dst_bf16,
+                               dst_pool_stride_pages, num_kv_heads, head_dim, page_size);
+    if (st != HMA_OK || n_pools == 0 || n_tokens == 0)
+        return st;
     const int rc = hma::launch_bfp8_rebuild_tiled(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens,
                                                   dst_bf16, dst_pages, dst_pool_stride_pages, num_kv_heads,
                                                   rope_reorder, static_cast<hipStream_t>(stream));
+    return rc == 0 ? HMA_OK : HMA_EHIP;
+}
+
+int hma_bfp8_pack_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
+                        int32_t n_shards, int32_t n_tokens, uint8_t *dst_mant, uint8_t *dst_exp,
+                        const int32_t *dst_pages, int64_t dst_pool_stride_pages, int32_t num_kv_heads,
+                        int32_t head_dim, int32_t page_size, void *stream)
+{
+    const int st = tiled_check(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens, dst_mant, dst_exp,
+                               dst_pool_stride_pages, num_kv_heads, head_dim, page_size);
+    if (st != HMA_OK || n_pools == 0 || n_tokens == 0)
+        return st;
+    if (dst_mant == dst_exp)
+        return HMA_EINVAL;
+    const int rc = hma::launch_bfp8_pack_tiled(src, src_pool_stride_bytes, n_pools, n_shards, n_tokens, dst_mant,
+                                               dst_exp, dst_pages, dst_pool_stride_pages, num_kv_heads,
+                                               static_cast<hipStream_t>(stream));
     return rc == 0 ? HMA_OK : HMA_EHIP;
 }
 
@@ -268,8 +305,8 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
                          int32_t max_pages_per_seq, const int32_t *context_lens,
                          int32_t max_context_len, int32_t batch, int32_t num_q_heads,
                          int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
-                         int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
-                         size_t workspace_bytes, void *stream)
+                         int32_t key_order, int32_t tokens_per_split, uint16_t *out, float *lse,
+                         void *workspace, size_t workspace_bytes, void *stream)
 {
     if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
         return HMA_EINVAL;
@@ -282,7 +319,7 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
         return HMA_EINVAL;
     if (max_pages_per_seq < 0 || (int64_t)max_context_len > (int64_t)max_pages_per_seq * page_size)
         return HMA_EINVAL;
-    if (!(scale == scale))
+    if (!(scale == scale) || (key_order != 0 && key_order != 1))
         return HMA_EINVAL;
     if (batch == 0)
         return HMA_OK;
@@ -326,6 +363,7 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
     a.n_splits = n_splits;
     a.waves = waves_for((int64_t)batch * num_kv_heads * n_splits);
     a.scale = scale;
+    a.key_interleaved = key_order;
     return hma::launch_decode_attn(a, static_cast<hipStream_t>(stream)) == 0 ? HMA_OK : HMA_EHIP;
 }
 

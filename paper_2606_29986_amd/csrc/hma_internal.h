@@ -31,6 +31,11 @@ int launch_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes,
                               int64_t dst_stride_pages, int32_t hkv, int32_t rope_reorder,
                               hipStream_t stream);
 
+// Tiled per-chip prefill shards -> BFP8 pages, bytes unchanged.
+int launch_bfp8_pack_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools, int32_t n_shards,
+                           int32_t n_tokens, uint8_t *dst_mant, uint8_t *dst_exp, const int32_t *dst_pages,
+                           int64_t dst_stride_pages, int32_t hkv, hipStream_t stream);
+
 // Host -> device copy of the staged pages on `stream`, then their rebuild
 // (src = staged page i, dst = dst_pages[i] or i when NULL).
 int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8_t *stage_mant,
@@ -49,6 +54,7 @@ struct AttnLaunch {
     void *workspace;
     int32_t max_pages, batch, hq, hkv, tps, n_splits;
     int32_t waves;          // 4 or 8 waves per workgroup
+    int32_t key_interleaved;  // K channels stored as rotary pairs (2i, 2i+1)
     float scale;
 };
 

@@ -89,6 +89,71 @@ __global__ __launch_bounds__(64 * kTiledWaves) void bfp8_rebuild_tiled_kernel(
     }
 }
 
+// The layout half of the pass, bytes unchanged: tiled shards -> BFP8 pages
+// (mantissa rows of 128 bytes, exponent rows of 8), for a decoder that keeps
+// raw BFP8 pages and decodes them inside attention.  Keys keep the interleaved
+// rotary order (a 16-channel block cannot be relabelled without re-encoding);
+// attention absorbs it by permuting the query.  Piece (row, q), q = 0..7, is
+// face row (channel tile q/2, face column q%2) of tile row `row`: 16 mantissa
+// bytes and the block's exponent byte; lane l takes pieces l + 64 s.
+__global__ __launch_bounds__(64 * kTiledWaves) void bfp8_pack_tiled_kernel(
+    const uint8_t *__restrict__ src, int64_t src_pool_stride_bytes, int64_t shard_bytes,
+    int32_t n_shards, int32_t heads_per_shard, int32_t token_tiles, int32_t n_tokens, int64_t n_units,
+    uint8_t *__restrict__ dst_mant, uint8_t *__restrict__ dst_exp, const int32_t *__restrict__ dst_pages,
+    int64_t dst_stride_pages, int32_t hkv)
+{
+    const int64_t unit = (int64_t)blockIdx.x * kTiledWaves + (threadIdx.x >> 6);
+    if (unit >= n_units)
+        return;
+    const int lane = threadIdx.x & 63;
+    const int tt = (int)(unit % token_tiles);
+    int64_t rest = unit / token_tiles;
+    const int h = (int)(rest % heads_per_shard);
+    rest /= heads_per_shard;
+    const int t = (int)(rest % n_shards);
+    const int64_t pool = rest / n_shards;
+    const uint8_t *tiles = src + pool * src_pool_stride_bytes + t * shard_bytes
+                           + ((int64_t)h * token_tiles + tt) * kChanTiles * kTileBytes;
+    const int q = lane & 7;
+    const uint8_t *tile = tiles + (q >> 1) * kTileBytes;
+    u32x4_t m[4];
+    uint32_t e[4];
+#pragma unroll
+    for (int s = 0; s < 4; s++) {
+        const int r = 8 * s + (lane >> 3);
+        const int face = 2 * (r >> 4) + (q & 1);
+        m[s] = *reinterpret_cast<const u32x4_t *>(tile + 64 + face * 256 + (r & 15) * 16);
+        e[s] = tile[face * 16 + (r & 15)];
+    }
+#pragma unroll
+    for (int s = 0; s < 4; s++) {
+        const int r = 8 * s + (lane >> 3);
+        const int token = 32 * tt + r;
+        if (token < n_tokens) {
+            const int32_t pidx = token / kPageSize;
+            const int64_t page = pool * dst_stride_pages + (dst_pages ? dst_pages[pidx] : pidx);
+            const int64_t row = (page * hkv + (int64_t)t * heads_per_shard + h) * kPageSize + token % kPageSize;
+            __builtin_nontemporal_store(m[s], reinterpret_cast<u32x4_t *>(dst_mant + row * kHeadDim + 16 * q));
+            dst_exp[row * kExpPerRow + q] = (uint8_t)e[s];
+        }
+    }
+}
+
+int launch_bfp8_pack_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools, int32_t n_shards,
+                           int32_t n_tokens, uint8_t *dst_mant, uint8_t *dst_exp, const int32_t *dst_pages,
+                           int64_t dst_stride_pages, int32_t hkv, hipStream_t stream)
+{
+    const int32_t hs = hkv / n_shards;
+    const int32_t token_tiles = (n_tokens + 31) / 32;
+    const int64_t shard_bytes = (int64_t)hs * token_tiles * kChanTiles * kTileBytes;
+    const int64_t n_units = (int64_t)n_pools * n_shards * hs * token_tiles;
+    const int64_t blocks = (n_units + kTiledWaves - 1) / kTiledWaves;
+    hipLaunchKernelGGL(bfp8_pack_tiled_kernel, dim3((unsigned)blocks), dim3(64 * kTiledWaves), 0, stream,
+                       src, src_pool_stride_bytes, shard_bytes, n_shards, hs, token_tiles, n_tokens, n_units,
+                       dst_mant, dst_exp, dst_pages, dst_stride_pages, hkv);
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
 int launch_bfp8_rebuild_tiled(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_pools,
                               int32_t n_shards, int32_t n_tokens, uint16_t *dst, const int32_t *dst_pages,
                               int64_t dst_stride_pages, int32_t hkv, int32_t rope_reorder,

@@ -55,7 +55,7 @@ class DevKV:
         B, Hq, D = kv.q.shape
         self.B, self.Hq, self.D = B, Hq, D
 
-    def attn(self, tokens_per_split=0, use_bf16_pools=None, with_lse=True, out=None):
+    def attn(self, tokens_per_split=0, use_bf16_pools=None, with_lse=True, out=None, key_order=0):
         B, Hq, D = self.B, self.Hq, self.D
         if out is None:
             out = torch.full((B, Hq, D), 0x7FC0, dtype=torch.int16, device="cuda")
@@ -67,7 +67,7 @@ class DevKV:
                              k_bf16=self.k_bf16 if use else None,
                              v_bf16=self.v_bf16 if use else None, lse=lse,
                              scale=self.kv.scale, num_kv_heads=self.kv.num_kv_heads,
-                             tokens_per_split=tokens_per_split, workspace=ws)
+                             tokens_per_split=tokens_per_split, workspace=ws, key_order=key_order)
         torch.cuda.synchronize()
         return out, lse
 

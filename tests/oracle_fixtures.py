@@ -26,10 +26,10 @@ class PagedKV:
     page_size: int
     scale: float
 
-    def oracle_attn(self):
+    def oracle_attn(self, key_order=0):
         return oracle.decode_attn(self.q, self.k_mant, self.k_exp, self.v_mant, self.v_exp,
                                   self.k_bf16, self.v_bf16, self.page_table, self.ctx,
-                                  self.num_kv_heads, self.page_size, self.scale)
+                                  self.num_kv_heads, self.page_size, self.scale, key_order=key_order)
 
 
 def make_paged(w: wl.Workload, layer: int = 0, ctx=None, bf16_fraction: float = 0.0,

@@ -26,7 +26,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["hma_bfp8_dequant_pages", "hma_bfp8_dequant_pages_naive",
-                            "hma_bfp8_rebuild_tiled", "hma_tiled_shard_bytes",
+                            "hma_bfp8_pack_tiled", "hma_bfp8_rebuild_tiled", "hma_tiled_shard_bytes",
                             "hma_decode_attn_bfp8",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
                             "hma_ingress_rebuild", "hma_status_string"])
@@ -165,15 +165,32 @@ def test_tiled_rebuild_validation():
     assert _tiled(pools=2, stride=need, dstride=0) == hma.HMA_EINVAL
 
 
+def test_pack_tiled_validation():
+    def _pack(**kw):
+        a = dict(src=FAKE, stride=0, pools=1, shards=4, n=100, dm=FAKE * 2, de=FAKE * 4, pages=None,
+                 dstride=0, hkv=8, D=128, P=16)
+        a.update(kw)
+        return hma.lib().hma_bfp8_pack_tiled(a["src"], a["stride"], a["pools"], a["shards"], a["n"],
+                                             a["dm"], a["de"], a["pages"], a["dstride"], a["hkv"],
+                                             a["D"], a["P"], None)
+    assert _pack(n=0) == hma.HMA_OK
+    assert _pack(shards=3) == hma.HMA_EINVAL
+    assert _pack(dm=None) == hma.HMA_EINVAL
+    assert _pack(de=MISALIGNED) == hma.HMA_EINVAL
+    assert _pack(de=FAKE * 2) == hma.HMA_EINVAL             # the two pools coincide
+    assert _pack(P=32) == hma.HMA_EUNSUPPORTED
+
+
 def _attn(**kw):
     a = dict(q=FAKE, km=FAKE, ke=FAKE, vm=FAKE, ve=FAKE, kb=None, vb=None, pt=FAKE, maxp=512,
              ctx=FAKE, maxctx=8192, B=16, Hq=64, Hkv=8, D=128, P=16, scale=0.088388346,
-             tps=0, out=FAKE, lse=None, ws=None, wsb=0)
+             tps=0, out=FAKE, lse=None, ws=None, wsb=0, korder=0)
     a.update(kw)
     return hma.lib().hma_decode_attn_bfp8(a["q"], a["km"], a["ke"], a["vm"], a["ve"], a["kb"],
                                           a["vb"], a["pt"], a["maxp"], a["ctx"], a["maxctx"],
                                           a["B"], a["Hq"], a["Hkv"], a["D"], a["P"], a["scale"],
-                                          a["tps"], a["out"], a["lse"], a["ws"], a["wsb"], None)
+                                          a["korder"], a["tps"], a["out"], a["lse"], a["ws"], a["wsb"],
+                                          None)
 
 
 def test_attn_validation():
@@ -192,6 +209,7 @@ def test_attn_validation():
     assert _attn(maxctx=-1) == hma.HMA_EINVAL
     assert _attn(maxp=100) == hma.HMA_EINVAL               # 8192 tokens need 512 pages
     assert _attn(scale=float("nan")) == hma.HMA_EINVAL
+    assert _attn(korder=2) == hma.HMA_EINVAL
     assert _attn(B=0) == hma.HMA_OK                        # nothing to do
     for k in ("q", "km", "ke", "vm", "ve", "pt", "ctx", "out"):
         assert _attn(**{k: None}) == hma.HMA_EINVAL, k

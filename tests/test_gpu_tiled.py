@@ -87,3 +87,86 @@ def test_tiled_rebuild_qwen3_32b_8k_request():
             oracle.rebuild_tiled(s, 0, 1, n_shards, n_tokens, hkv, want,
                                  np.arange(n_req, dtype=np.int32), 0, kind == 0)
             assert np.array_equal(out[kind, layer].cpu().numpy().view(np.uint16), want), (kind, layer)
+
+
+@pytest.mark.parametrize("n_shards,n_tokens", [(1, 1), (2, 47), (4, 300), (8, 64)])
+def test_pack_tiled_matches_oracle(n_shards, n_tokens):
+    note(f"pack tiled: shards={n_shards} tokens={n_tokens}")
+    rng = np.random.default_rng(900 + n_tokens + n_shards)
+    hkv, n_pools, pool_pages = 8, 2, 30
+    src, stride, dst_pages = _case(rng, n_pools, n_shards, n_tokens, hkv, pool_pages, pad_stride=16)
+    wm = np.full((n_pools * pool_pages, hkv, P, D), 0xA5, np.uint8)
+    we = np.full((n_pools * pool_pages, hkv, P, D // 16), 0xA5, np.uint8)
+    oracle.pack_tiled(src, stride, n_pools, n_shards, n_tokens, hkv, wm, we, dst_pages, pool_pages)
+    gm = torch.full(wm.shape, 0xA5, dtype=torch.uint8, device="cuda")
+    ge = torch.full(we.shape, 0xA5, dtype=torch.uint8, device="cuda")
+    hma.bfp8_pack_tiled(dev(src), gm, ge, n_tokens, n_shards, dst_pages=dev(dst_pages), n_pools=n_pools,
+                        src_pool_stride_bytes=stride, dst_pool_stride_pages=pool_pages, num_kv_heads=hkv)
+    torch.cuda.synchronize()
+    assert np.array_equal(gm.cpu().numpy(), wm)
+    assert np.array_equal(ge.cpu().numpy(), we)
+
+
+def test_raw_pages_from_shards_through_fused_attention():
+    """The deferred path end to end: prefill shards packed into BFP8 pages on
+    the GPU, keys still in the interleaved rotary order, read by the fused
+    attention with key_order = 1; against the oracle (which relabels the keys
+    on read).  Both kernel shapes; also bitwise equal to the mixed-format
+    kernel over BF16 pages that hold the same (stored-order) keys."""
+    import workloads as wl
+    from gpu_util import DevKV, assert_attn_close
+    from oracle_fixtures import PagedKV
+    rng = np.random.default_rng(4242)
+    B, hq, hkv, n_shards = 4, 32, 8, 4
+    ctx = np.array([70, 200, 1, 129], np.int32)
+    pages_per = (ctx + P - 1) // P
+    total = int(pages_per.sum())
+    pt = np.zeros((B, int(pages_per.max())), np.int32)
+    order = rng.permutation(total).astype(np.int32)
+    k_mant = np.zeros((total, hkv, P, D), np.uint8)
+    k_exp = np.zeros((total, hkv, P, D // 16), np.uint8)
+    v_mant = np.zeros_like(k_mant)
+    v_exp = np.zeros_like(k_exp)
+    at = 0
+    for b in range(B):
+        ids = order[at:at + pages_per[b]]
+        at += pages_per[b]
+        pt[b, :pages_per[b]] = ids
+        for mant, ex in ((k_mant, k_exp), (v_mant, v_exp)):
+            # one request's shards: moderate exponents, random bytes
+            pool_bytes = n_shards * hma.tiled_shard_bytes(int(ctx[b]), hkv // n_shards)
+            src = rng.integers(0, 256, pool_bytes, dtype=np.uint8)
+            tiles = src.reshape(-1, 1088)
+            tiles[:, :64] = rng.integers(118, 132, (tiles.shape[0], 64), dtype=np.uint8)
+            gm = torch.zeros(mant.shape, dtype=torch.uint8, device="cuda")
+            ge = torch.zeros(ex.shape, dtype=torch.uint8, device="cuda")
+            gm.copy_(torch.from_numpy(mant))
+            ge.copy_(torch.from_numpy(ex))
+            hma.bfp8_pack_tiled(dev(src), gm, ge, int(ctx[b]), n_shards, dst_pages=dev(ids),
+                                num_kv_heads=hkv)
+            torch.cuda.synchronize()
+            mant[:] = gm.cpu().numpy()
+            ex[:] = ge.cpu().numpy()
+            # the GPU packing is pinned separately; check this request's pages anyway
+            wm = np.zeros_like(mant)
+            we = np.zeros_like(ex)
+            oracle.pack_tiled(src, 0, 1, n_shards, int(ctx[b]), hkv, wm, we, ids, 0)
+            for i, pid in enumerate(ids):
+                n_valid = min(P, int(ctx[b]) - i * P)
+                assert np.array_equal(mant[pid, :, :n_valid], wm[pid, :, :n_valid])
+    q = wl.f32_to_bf16_bits(rng.standard_normal((B, hq, D)).astype(np.float32))
+    kv = PagedKV(q, k_mant, k_exp, v_mant, v_exp, oracle.decode_blocks(k_mant, k_exp),
+                 oracle.decode_blocks(v_mant, v_exp), pt, ctx, hkv, P, 1.0 / np.sqrt(D))
+    ref, ref_lse = kv.oracle_attn(key_order=1)
+    d = DevKV(kv)
+    for tps in (0, 16):        # 32 workgroups (8 waves each) and 416 (the 4-wave shape)
+        note(f"attn over packed shards, key_order=1, tps={tps}")
+        out, lse = d.attn(tokens_per_split=tps, use_bf16_pools=False, key_order=1)
+        assert_attn_close(out, lse, ref, ref_lse, what=f"interleaved keys tps={tps}")
+        kv_bf = PagedKV(q, k_mant, k_exp, v_mant, v_exp, kv.k_bf16, kv.v_bf16, pt | wl.TAG_BF16, ctx,
+                        hkv, P, kv.scale)
+        out_b, lse_b = DevKV(kv_bf).attn(tokens_per_split=tps, key_order=1)
+        assert torch.equal(out, out_b) and torch.equal(lse, lse_b)
+    # and the interleaved keys do matter: reading them as half-split differs
+    out0, _ = d.attn(use_bf16_pools=False, key_order=0)
+    assert not torch.equal(out0, out)
