@@ -195,3 +195,17 @@ def test_full_size_workload_sampled(index, n_seq):
     ref, ref_lse = _oracle_rows(kv, seqs)
     err = assert_attn_close(out, lse, ref, ref_lse, rows=seqs, what=w.name)
     note(f"attn: {w.name} max abs err {err:.3g} on {len(seqs)} sequences")
+
+
+def test_single_long_sequence_many_splits():
+    """One 32K-token sequence (Qwen3-32B heads): the automatic split gives 32
+    splits of 1024 tokens on 256 one-per-CU workgroups, so the last workgroup
+    of each KV head folds 32 partials."""
+    w = tiny_workload(Hq=64, Hkv=8, B=1, index=6)
+    ctx = [32768]
+    assert hma.tokens_per_split(1, 64, 8, 32768) == 1024
+    note(f"attn: single sequence ctx={ctx}")
+    kv = make_paged(w, ctx=ctx)
+    ref, ref_lse = kv.oracle_attn()
+    out, lse = DevKV(kv).attn()
+    assert_attn_close(out, lse, ref, ref_lse, what="32K single sequence")

@@ -129,8 +129,21 @@ def bf16_page_mask(w: Workload, total_pages: int, fraction: float | None = None)
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """float32 -> BF16 bit patterns, round to nearest even (finite inputs)."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    rounding = ((u >> 16) & 1) + np.uint32(0x7FFF)
-    return ((u + rounding) >> 16).astype(np.uint16)
+    flat = u.reshape(-1)
+    out = np.empty(flat.size, np.uint16)
+    # in chunks, in place: large fresh temporaries dominate the cost otherwise
+    step = 1 << 18
+    tmp = np.empty(min(step, flat.size), np.uint32)
+    for s in range(0, flat.size, step):
+        c = flat[s:s + step]
+        t = tmp[:c.size]
+        np.right_shift(c, 16, out=t)
+        t &= 1
+        t += np.uint32(0x7FFF)
+        t += c
+        t >>= 16
+        out[s:s + step] = t
+    return out.reshape(u.shape)
 
 
 def kv_values_bf16(w: Workload, layer: int, kind: str, num_pages: int) -> np.ndarray:
@@ -147,7 +160,8 @@ def kv_values_bf16(w: Workload, layer: int, kind: str, num_pages: int) -> np.nda
         r = rng(w.index, "outlier", layer, kv_id)
         for j in range(w.num_kv_heads):
             ch = r.choice(w.head_dim, size=4, replace=False)
-            x[:, j, :, ch] *= np.float32(20.0)
+            for c in ch:           # distinct channels; strided views, no temporaries
+                x[:, j, :, c] *= np.float32(20.0)
     elif w.kv_dist == "channel_lognormal":
         r = rng(w.index, "chanscale", layer, kv_id)
         s = r.lognormal(0.0, 0.5, size=(w.num_kv_heads, w.head_dim)).astype(np.float32)
