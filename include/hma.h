@@ -36,9 +36,8 @@
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream).
  *     No call synchronises or allocates.
  *   - Arguments are validated on the host before any HIP call; a rejected
- *     call enqueues nothing.  Device-resident contents (page ids in range,
- *     context_lens[b] <= max_context_len) are the caller's contract; breaking
- *     it is undefined behaviour.
+ *     call enqueues nothing.  Device-resident contents (page ids in range)
+ *     are the caller's contract; breaking it is undefined behaviour.
  *   - Return value: HMA_OK, or a negative hma_status.  HMA_EHIP means the
  *     launch itself failed.
  */
@@ -223,7 +222,11 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  * BF16 values of tagged pages).  Products and sums use float32; the context
  * is split into ranges of tokens_per_split tokens handled by separate
  * workgroups whose partial (max, sum, weighted values) are merged exactly by
- * log-sum-exp.  context_lens[b] == 0 gives out = 0 and lse = -inf.  Slots at
+ * log-sum-exp.  When the splits outnumber what the chip runs at once, the
+ * kernel orders them itself from the device-resident lengths (full splits
+ * level by level, then the shorter last splits), so a ragged batch needs no
+ * host-side length information; the order does not change the result.
+ * context_lens[b] == 0 gives out = 0 and lse = -inf.  Slots at
  * or past the context end in the last page are never used, whatever they
  * hold.
  *
@@ -234,7 +237,8 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *              set.  When NULL the HMA_PAGE_BF16 bit is ignored and every
  *              page is read from the BFP8 pools.
  *   page_table int32 [batch][max_pages_per_seq]
- *   context_lens  int32 [batch], each in [0, max_context_len]
+ *   context_lens  int32 [batch], each >= 0; a length above max_context_len
+ *              is read as max_context_len
  *   max_context_len  host-side bound that sizes the launch (no device read
  *              on the host); must be <= max_pages_per_seq * page_size
  *   num_q_heads % num_kv_heads == 0 and num_q_heads / num_kv_heads <= 16;

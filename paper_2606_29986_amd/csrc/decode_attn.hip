@@ -40,6 +40,9 @@
 // splits' partials, in split order, with device-coherent loads (log-sum-exp).
 // No cache-wide writeback or invalidate is involved (on this multi-XCD part
 // an agent-scope fence writes back and invalidates the whole L2).
+#include <algorithm>
+#include <atomic>
+
 #include "hma_device.h"
 #include "hma_internal.h"
 
@@ -68,6 +71,8 @@ struct AttnParams {
     float2 *part_ml;
     float *part_o;
     int32_t max_pages, batch, hq, hkv, g, tps, n_splits;
+    int32_t max_ctx;          // context lengths are clamped to this bound
+    int32_t planned;          // 1: length-aware persistent schedule (4-wave shape)
     int32_t key_interleaved;
     float scale_log2;
 };
@@ -356,6 +361,29 @@ __device__ __forceinline__ float max_over_groups(float x)
     return fmaxf(__uint_as_float(c[0]), __uint_as_float(c[1]));
 }
 
+// Sum over the same four lane groups: (x_l + x_l^16) + (the same at l^32),
+// identical in all four lanes.
+__device__ __forceinline__ float sum_over_groups(float x)
+{
+    const uint32_t u = __float_as_uint(x);
+    const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+    const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    const uint32_t v = __float_as_uint(y);
+    const auto c = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __uint_as_float(c[0]) + __uint_as_float(c[1]);
+}
+
+// threadIdx.x through an opaque move.  In the persistent schedule the split
+// body runs in a loop; without this the compiler hoists lane-derived
+// addresses and constants out of the loop and keeps them live across it,
+// which costs the registers of a third workgroup per CU.
+__device__ __forceinline__ int thread_index()
+{
+    int t;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"((int)threadIdx.x));
+    return t;
+}
+
 struct SoftmaxState {
     float m;       // running max of scaled scores (log2 units), head r
     float l;       // this lane's share of the running sum of weights, head r
@@ -538,17 +566,36 @@ __device__ __forceinline__ WavePages wave_pages(int n_pages, int wave)
     return WavePages{first, end > first ? (end - first + 3) / 4 : 0};
 }
 
-template <bool MIXED, int WAVES>
-__global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnParams p)
+// Zero output (and lse = -inf) for the query heads of KV head j of an empty
+// sequence b; one wave.
+__device__ __forceinline__ void zero_pair_output(const AttnParams &p, int b, int j)
 {
-    const int id = blockIdx.x;
-    const int j = id % p.hkv;
-    const int b = (id / p.hkv) % p.batch;
-    const int s = id / (p.hkv * p.batch);
-    const int ctx = p.ctx_lens[b];
-    // the wave index is uniform: page bookkeeping stays in scalar registers
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
+    const int G = lane >> 4;
+    const int r = lane & 15;
+    if (r >= p.g)
+        return;
+    const int64_t out_row = (int64_t)b * p.hq + j * p.g + r;
+    const u32x4_t z = {0u, 0u, 0u, 0u};
+    uint16_t *o = p.out + out_row * kHeadDim + 32 * G;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+        *reinterpret_cast<u32x4_t *>(o + 8 * i) = z;
+    if (p.lse && G == 0)
+        p.lse[out_row] = -INFINITY;
+}
+
+// One split: the tokens [s*tps, min(ctx, (s+1)*tps)) of sequence b, KV head j
+// (non-empty).  Every wave of the workgroup calls it, and every wave meets the
+// same barriers; waves other than 0 leave after the workgroup merge.
+template <bool MIXED, int WAVES>
+__device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, int s, int ctx,
+                                             uint8_t *sm_buf, uint32_t *sm_pt)
+{
+    const int tid = thread_index();
+    // the wave index is uniform: page bookkeeping stays in scalar registers
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
     const int G = lane >> 4;
     const int r = lane & 15;
     const bool head_ok = r < p.g;
@@ -556,31 +603,14 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
     const int64_t out_row = (int64_t)b * p.hq + head;
 
     const int t_begin = s * p.tps;
-    if (t_begin >= ctx) {
-        // empty split; split 0 of an empty sequence owns its (zero) output
-        if (s == 0 && wave == 0 && head_ok) {
-            u32x4_t z = {0u, 0u, 0u, 0u};
-            uint16_t *o = p.out + out_row * kHeadDim + 32 * G;
-#pragma unroll
-            for (int i = 0; i < 4; i++)
-                *reinterpret_cast<u32x4_t *>(o + 8 * i) = z;
-            if (p.lse && G == 0)
-                p.lse[out_row] = -INFINITY;
-        }
-        return;
-    }
     const int n_tok = min(ctx, t_begin + p.tps) - t_begin;
     const int n_split_b = (ctx + p.tps - 1) / p.tps;
     const int n_pages = (n_tok + kPageSize - 1) / kPageSize;
 
-    // LDS: the wave merge, and this split's slice of the page table
-    __shared__ __attribute__((aligned(16))) uint8_t sm_buf[merge_bytes<WAVES>()];
-    __shared__ uint32_t sm_pt[kMaxSplitPages];
-
     // stage this split's page-table slice in LDS
     {
         const int32_t *pt = p.page_table + (int64_t)b * p.max_pages + t_begin / kPageSize;
-        for (int i = threadIdx.x; i < n_pages; i += 64 * WAVES)
+        for (int i = tid; i < n_pages; i += 64 * WAVES)
             sm_pt[i] = (uint32_t)pt[i];
     }
 
@@ -649,9 +679,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
     // ---- merge the waves of the workgroup through LDS, as a fixed binary
     //      tree (waves h..2h-1 hand their partial to waves 0..h-1), so every
     //      wave takes part and the result does not depend on timing
-    float L = st.l;
-    L += __shfl_xor(L, 16);
-    L += __shfl_xor(L, 32);
+    float L = sum_over_groups(st.l);
     float M = st.m;
     f32x4_t *sm_o = reinterpret_cast<f32x4_t *>(sm_buf);
     float2 *sm_ml = reinterpret_cast<float2 *>(sm_buf + (WAVES - 1) * kMergeSlotBytes);
@@ -724,7 +752,7 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
     if (lane == 0)
         last = __hip_atomic_fetch_add(&p.tickets[pair_id], 1, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT) == n_split_b - 1;
-    last = __shfl(last, 0);
+    last = __builtin_amdgcn_readfirstlane(last);
     if (!last)
         return;
 
@@ -784,6 +812,223 @@ __global__ __launch_bounds__(64 * WAVES, 2) void decode_attn_bfp8_kernel(AttnPar
         __hip_atomic_store(&p.tickets[pair_id], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ------------------------------------------------------- the split schedule
+//
+// Direct: workgroup id = (s * batch + b) * hkv + j owns split s of (b, j);
+// the grid covers every split the longest possible sequence could have, and
+// workgroups past their sequence's end leave at once.
+//
+// Planned (4-wave shape, for batches whose lengths the host does not know):
+// the grid is twice the workgroups the chip holds at once, and every
+// workgroup derives the same list of splits from the context lengths:
+//   1. the full splits (tps tokens) level by level: level s holds split s of
+//      every sequence with more than s full splits, in sequence order;
+//   2. every sequence's shorter last split, in sequence order;
+// each entry for all KV heads (KV head fastest).  Workgroup w takes entries
+// w, w + grid, ...  No workgroup is spent on a split that does not exist,
+// the short pieces come last, and the splits of one (sequence, KV head)
+// pair lie far apart in the list, so they do not all finish (and take their
+// tickets) at once.  A split's arithmetic does not depend on which workgroup
+// runs it, so both schedules give the same bits.
+
+// Count of n < limit with pre[n + 1] <= k, for a nondecreasing table pre:
+// the row whose range [pre[n], pre[n + 1]) holds k.
+__device__ __forceinline__ int row_of(const int32_t *pre, int limit, int k)
+{
+    int n = 0;
+    for (int n0 = 0; n0 < limit; n0 += 64) {
+        const int i = n0 + (thread_index() & 63);
+        const uint64_t le = __ballot(i < limit && pre[i + 1] <= k);
+        n += __popcll(le);
+        if (le != ~0ull)
+            break;
+    }
+    return __builtin_amdgcn_readfirstlane(n);
+}
+
+// The i-th (from 0) sequence, in sequence order, with more than s full splits
+// (a context of at least (s + 1) * tps tokens).
+__device__ __forceinline__ int nth_longer(const int32_t *sm_ctx, int batch, int tps, int s, int i)
+{
+    const int lane = thread_index() & 63;
+    const int need = (s + 1) * tps;
+    for (int b0 = 0; b0 < batch; b0 += 64) {
+        const int b = b0 + lane;
+        const uint64_t m = __ballot(b < batch && sm_ctx[b] >= need);
+        const int cnt = __popcll(m);
+        if (i < cnt) {
+            const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+            const uint64_t hit = __ballot(((m >> lane) & 1) && below == i);
+            return __builtin_amdgcn_readfirstlane(b0 + __builtin_ctzll(hit));
+        }
+        i -= cnt;
+    }
+    return 0;     // not reached for an entry of the list
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave (row shifts within each
+// 16-lane row, then the row totals broadcast to the rows above).
+__device__ __forceinline__ int wave_inclusive_scan(int x)
+{
+    x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);     // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);     // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);     // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);     // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);    // row_bcast:15
+    x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);    // row_bcast:31
+    return x;
+}
+
+struct Plan {
+    int n_full;     // full splits over all sequences
+    int n_last;     // shorter last splits
+};
+
+// True when every sequence has the context length c0 (each wave decides for
+// itself; all waves reach the same answer).
+__device__ __forceinline__ bool all_lengths_equal(const AttnParams &p, int c0)
+{
+    const int lane = thread_index() & 63;
+    for (int b0 = 0; b0 < p.batch; b0 += 64) {
+        const int b = b0 + lane;
+        const int c = b < p.batch ? min(p.ctx_lens[b], p.max_ctx) : c0;
+        if (__ballot(c != c0))
+            return false;
+    }
+    return true;
+}
+
+// The list's tables, from the context lengths; wave 0 of every workgroup
+// builds its own copy in LDS, 64 entries at a time:
+//   sm_ctx[b]    context length of sequence b (clamped to the host bound);
+//   sm_last[b]   shorter last splits of the sequences before b (b <= batch);
+//   sm_level[s]  full splits in the levels before s (s <= n_splits).  Level s
+//                has C(s) = #{b : nfull_b > s} entries, taken from the
+//                histogram of nfull: C(s) = #{nfull >= 1} - #{1 <= nfull <= s}.
+__device__ __forceinline__ Plan build_plan(const AttnParams &p, int32_t *sm_ctx, int32_t *sm_last,
+                                           int32_t *sm_level)
+{
+    const int n_lv = p.n_splits;     // nfull_b <= n_splits < kPlanMaxBatch (host)
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        for (int s0 = 0; s0 <= n_lv; s0 += 64)
+            if (s0 + lane <= n_lv)
+                sm_level[s0 + lane] = 0;
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+        int n_last = 0, n_long = 0;
+        for (int b0 = 0; b0 < p.batch; b0 += 64) {
+            const int b = b0 + lane;
+            const int c = b < p.batch ? min(p.ctx_lens[b], p.max_ctx) : 0;
+            const int f = c / p.tps;
+            const uint64_t has_last = __ballot(c - f * p.tps > 0);
+            if (b < p.batch) {
+                sm_ctx[b] = c;
+                sm_last[b] = n_last + (int)__builtin_amdgcn_mbcnt_hi(
+                                          (uint32_t)(has_last >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)has_last, 0u));
+            }
+            if (f > 0)
+                atomicAdd(&sm_level[f], 1);
+            n_last += __popcll(has_last);
+            n_long += __popcll(__ballot(f > 0));
+        }
+        if (lane == 0)
+            sm_last[p.batch] = n_last;
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+        int below = 0, acc = 0;
+        for (int s0 = 0; s0 <= n_lv; s0 += 64) {
+            const int s = s0 + lane;
+            const int h = s <= n_lv ? sm_level[s] : 0;
+            const int hs = wave_inclusive_scan(h);
+            const int cnt = n_long - (below + hs);          // C(s)
+            const int cs = wave_inclusive_scan(cnt);
+            if (s <= n_lv)
+                sm_level[s] = acc + cs - cnt;
+            below += __builtin_amdgcn_readlane(hs, 63);
+            acc += __builtin_amdgcn_readlane(cs, 63);
+        }
+    }
+    __syncthreads();
+    Plan plan;
+    plan.n_full = __builtin_amdgcn_readfirstlane(sm_level[n_lv]);
+    plan.n_last = __builtin_amdgcn_readfirstlane(sm_last[p.batch]);
+    return plan;
+}
+
+// Occupancy: the 4-wave pure-BFP8 kernel is built for three workgroups per CU
+// (at most 168 registers per lane); the others for two waves per SIMD.
+template <bool MIXED, int WAVES>
+__global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void decode_attn_bfp8_kernel(
+    AttnParams p)
+{
+    // LDS: the wave merge, and the current split's slice of the page table
+    __shared__ __attribute__((aligned(16))) uint8_t sm_buf[merge_bytes<WAVES>()];
+    __shared__ uint32_t sm_pt[kMaxSplitPages];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+
+    if constexpr (WAVES == 4) {
+        if (p.planned) {
+            __shared__ int32_t sm_ctx[kPlanMaxBatch], sm_last[kPlanMaxBatch + 1];
+            __shared__ int32_t sm_level[kPlanMaxBatch];
+            // equal lengths need no tables: the list is then split-major,
+            // entry k = split k / batch of sequence k % batch
+            const int c0 = min(p.ctx_lens[0], p.max_ctx);
+            const bool uniform = all_lengths_equal(p, c0);
+            const int nf0 = c0 / p.tps;
+            Plan plan;
+            if (uniform) {
+                plan.n_full = nf0 * p.batch;
+                plan.n_last = c0 > nf0 * p.tps ? p.batch : 0;
+            } else {
+                plan = build_plan(p, sm_ctx, sm_last, sm_level);
+            }
+            const int n_items = (plan.n_full + plan.n_last) * p.hkv;
+            // empty sequences own a zero output
+            for (int b = blockIdx.x; b < p.batch; b += gridDim.x)
+                if ((uniform ? c0 : __builtin_amdgcn_readfirstlane(sm_ctx[b])) == 0)
+                    for (int j = wave; j < p.hkv; j += WAVES)
+                        zero_pair_output(p, b, j);
+            for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+                const int k = it / p.hkv;
+                const int j = it - k * p.hkv;
+                int b, s, ctx;
+                if (uniform) {
+                    s = k < plan.n_full ? k / p.batch : nf0;
+                    b = k < plan.n_full ? k - s * p.batch : k - plan.n_full;
+                    ctx = c0;
+                } else {
+                    if (k < plan.n_full) {
+                        s = row_of(sm_level, p.n_splits, k);
+                        b = nth_longer(sm_ctx, p.batch, p.tps, s,
+                                       k - __builtin_amdgcn_readfirstlane(sm_level[s]));
+                    } else {
+                        b = row_of(sm_last, p.batch, k - plan.n_full);
+                    }
+                    ctx = __builtin_amdgcn_readfirstlane(sm_ctx[b]);
+                    if (k >= plan.n_full)
+                        s = ctx / p.tps;
+                }
+                attend_split<MIXED, WAVES>(p, b, j, s, ctx, sm_buf, sm_pt);
+            }
+            return;
+        }
+    }
+
+    const int id = blockIdx.x;
+    const int j = id % p.hkv;
+    const int b = (id / p.hkv) % p.batch;
+    const int s = id / (p.hkv * p.batch);
+    const int ctx = min(p.ctx_lens[b], p.max_ctx);
+    if (s * p.tps >= ctx) {
+        // empty split; split 0 of an empty sequence owns its (zero) output
+        if (s == 0 && wave == 0)
+            zero_pair_output(p, b, j);
+        return;
+    }
+    attend_split<MIXED, WAVES>(p, b, j, s, ctx, sm_buf, sm_pt);
+}
+
 size_t attn_workspace_bytes(int32_t batch, int32_t hq, int32_t hkv, int32_t n_splits)
 {
     if (n_splits <= 1)
@@ -794,6 +1039,30 @@ size_t attn_workspace_bytes(int32_t batch, int32_t hq, int32_t hkv, int32_t n_sp
     const size_t ml = (pairs * n_splits * g * sizeof(float2) + 255) & ~(size_t)255;
     const size_t o = pairs * n_splits * g * kHeadDim * sizeof(float);
     return tickets + ml + o;
+}
+
+// Workgroups of the 4-wave kernel the whole chip holds at once (occupancy per
+// compute unit times compute units), queried once per device and variant.
+int resident_workgroups(bool mixed)
+{
+    constexpr int kMaxDevices = 64;
+    static std::atomic<int> cache[kMaxDevices][2];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return 0;
+    int n = cache[dev][mixed].load(std::memory_order_relaxed);
+    if (n > 0)
+        return n;
+    int per_cu = 0, cus = 0;
+    const hipError_t e =
+        mixed ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_attn_bfp8_kernel<true, 4>, 256, 0)
+              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_attn_bfp8_kernel<false, 4>, 256, 0);
+    if (e != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    n = per_cu * cus;
+    cache[dev][mixed].store(n, std::memory_order_relaxed);
+    return n;
 }
 
 int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
@@ -817,6 +1086,8 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
     p.g = a.hq / a.hkv;
     p.tps = a.tps;
     p.n_splits = a.n_splits;
+    p.max_ctx = a.max_ctx;
+    p.planned = a.planned;
     p.key_interleaved = a.key_interleaved;
     p.scale_log2 = a.scale * kLog2e;
     p.tickets = nullptr;
@@ -834,7 +1105,13 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
     }
     const int64_t blocks = (int64_t)a.batch * a.hkv * a.n_splits;
     const bool mixed = a.k_bf16 != nullptr && a.v_bf16 != nullptr;
-    const dim3 grid((unsigned)blocks);
+    dim3 grid((unsigned)blocks);
+    if (a.planned) {
+        const int64_t resident = resident_workgroups(mixed);
+        if (resident < 1)
+            return -1;
+        grid = dim3((unsigned)std::min(blocks, 2 * resident));
+    }
     if (a.waves == 8) {
         if (mixed)
             hipLaunchKernelGGL((decode_attn_bfp8_kernel<true, 8>), grid, dim3(512), 0, stream, p);

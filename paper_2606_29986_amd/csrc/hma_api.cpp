@@ -361,7 +361,9 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
     a.hkv = num_kv_heads;
     a.tps = tps;
     a.n_splits = n_splits;
+    a.max_ctx = max_context_len;
     a.waves = waves_for((int64_t)batch * num_kv_heads * n_splits);
+    a.planned = a.waves == 4 && batch <= hma::kPlanMaxBatch && n_splits < hma::kPlanMaxBatch;
     a.scale = scale;
     a.key_interleaved = key_order;
     return hma::launch_decode_attn(a, static_cast<hipStream_t>(stream)) == 0 ? HMA_OK : HMA_EHIP;

@@ -11,6 +11,10 @@ namespace hma {
 // in LDS (4 bytes per 16-token page).
 constexpr int32_t kMaxTokensPerSplit = 16384;
 constexpr int kMaxSplitPages = kMaxTokensPerSplit / 16;
+// Largest batch, and bound on the splits per sequence, that the length-aware
+// schedule handles (its tables sit in LDS); beyond them the direct schedule
+// runs.
+constexpr int kPlanMaxBatch = 1024;
 
 // Returns 0 on a successful launch, -1 if the launch failed.  src_pages or
 // dst_pages may be NULL (identity).
@@ -53,7 +57,9 @@ struct AttnLaunch {
     float *lse;
     void *workspace;
     int32_t max_pages, batch, hq, hkv, tps, n_splits;
+    int32_t max_ctx;        // host bound on the context lengths (longer ones are clamped)
     int32_t waves;          // 4 or 8 waves per workgroup
+    int32_t planned;        // length-aware persistent schedule (4 waves, batch <= kPlanMaxBatch)
     int32_t key_interleaved;  // K channels stored as rotary pairs (2i, 2i+1)
     float scale;
 };

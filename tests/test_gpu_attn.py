@@ -209,3 +209,64 @@ def test_single_long_sequence_many_splits():
     ref, ref_lse = kv.oracle_attn()
     out, lse = DevKV(kv).attn()
     assert_attn_close(out, lse, ref, ref_lse, what="32K single sequence")
+
+
+def _attn_with_bound(d, max_ctx, tps):
+    """d.attn with a looser host bound on the context lengths (page table
+    padded to match): the bound sizes the grid and the workspace, not the
+    result."""
+    kv = d.kv
+    cols = (max_ctx + 15) // 16
+    pt = np.zeros((kv.page_table.shape[0], max(cols, kv.page_table.shape[1])), np.int32)
+    pt[:, :kv.page_table.shape[1]] = kv.page_table
+    out = torch.full((d.B, d.Hq, d.D), 0x7FC0, dtype=torch.int16, device="cuda")
+    lse = torch.full((d.B, d.Hq), float("nan"), dtype=torch.float32, device="cuda")
+    ws = hma.alloc_workspace(d.B, d.Hq, kv.num_kv_heads, max_ctx, tps)
+    hma.decode_attn_bfp8(d.q, d.k_mant, d.k_exp, d.v_mant, d.v_exp, dev(pt), d.ctx, max_ctx, out, lse=lse,
+                         scale=kv.scale, num_kv_heads=kv.num_kv_heads, tokens_per_split=tps, workspace=ws)
+    torch.cuda.synchronize()
+    return out, lse
+
+
+@pytest.mark.parametrize("lengths", ["ragged", "equal", "equal_whole"])
+def test_length_aware_schedule_many_sequences_and_levels(lengths):
+    """A batch the host sees only through its longest length: 70 sequences
+    (more than one wave's worth) from empty to 4500 tokens, split every 32
+    tokens (141 split levels); also 70 equal lengths (the schedule's
+    table-free case), with and without a shorter last split.  Against the
+    oracle, and bitwise equal to the direct one-workgroup-per-split schedule
+    (reached through a looser length bound that gives 1024 splits per
+    sequence)."""
+    rng = np.random.default_rng(70)
+    w = tiny_workload(Hq=16, Hkv=2, B=70, index=7)
+    if lengths == "ragged":
+        ctx = rng.integers(0, 300, 70).astype(np.int32)
+        ctx[[3, 40]] = [4500, 2100]
+        ctx[[5, 6, 7]] = [0, 1, 32]
+    else:
+        ctx = np.full(70, 300 if lengths == "equal" else 320, np.int32)
+    tps = 32
+    assert hma.tokens_per_split(70, 16, 2, int(ctx.max())) != tps        # a forced split length
+    note(f"attn: length-aware schedule, B=70, {lengths}, max ctx {ctx.max()}, tps {tps}")
+    kv = make_paged(w, ctx=ctx)
+    ref, ref_lse = kv.oracle_attn()
+    d = DevKV(kv)
+    out, lse = d.attn(tokens_per_split=tps)
+    assert_attn_close(out, lse, ref, ref_lse, what="length-aware schedule")
+    note("attn: direct schedule through a looser bound")
+    out_d, lse_d = _attn_with_bound(d, 1024 * tps, tps)
+    assert torch.equal(out, out_d) and torch.equal(lse, lse_d)
+
+
+def test_batch_beyond_the_schedule_tables():
+    """1030 sequences (more than the length-aware schedule's tables hold):
+    the direct schedule runs; against the oracle."""
+    rng = np.random.default_rng(1030)
+    w = tiny_workload(Hq=8, Hkv=1, B=1030, index=8)
+    ctx = rng.integers(0, 60, 1030).astype(np.int32)
+    note("attn: batch of 1030 sequences")
+    kv = make_paged(w, ctx=ctx)
+    ref, ref_lse = kv.oracle_attn()
+    for tps in (0, 16):
+        out, lse = DevKV(kv).attn(tokens_per_split=tps)
+        assert_attn_close(out, lse, ref, ref_lse, what=f"B=1030 tps={tps}")
