@@ -33,11 +33,13 @@
 //        leaves lane (G, r) with head r, channels 32G..32G+31 -- the same head
 //        as its softmax state, so the online rescale needs no data movement.
 //
-// Split merge.  The four waves are merged through LDS.  With more than one
-// split, each workgroup publishes (max, sum, weighted values) with
-// device-coherent (sc1) stores, waits for them to complete, and takes a ticket
-// with a device-scope atomic; the last workgroup of (b, j) folds all the
-// splits' partials, in split order, with device-coherent loads (log-sum-exp).
+// Split merge.  The waves leave their partials in LDS and each wave combines
+// one (or two) of the eight accumulator columns of all of them.  With more
+// than one split, every wave publishes its columns of the workgroup's
+// (max, sum, weighted values) with device-coherent (sc1) stores, the stores
+// complete, and one device-scope atomic takes a ticket; in the last workgroup
+// of (b, j) each wave folds its columns of all the splits' partials, in split
+// order, with device-coherent loads (log-sum-exp).
 // No cache-wide writeback or invalidate is involved (on this multi-XCD part
 // an agent-scope fence writes back and invalidates the whole L2).
 #include <algorithm>
@@ -112,20 +114,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void *base)
 __device__ __forceinline__ int qk_channel(int G, int kk)
 {
     return (kk >> 1) * 64 + 16 * G + (kk & 1) * 8;
-}
-
-// Write 32 channels of one head as BF16: o[n][i] is channel 32G + 8i + n.
-__device__ __forceinline__ void store_out_row(uint16_t *dst, const f32x4_t (&o)[8], float inv)
-{
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-        u32x4_t v;
-        v.x = pack_bf16_rne(o[0][i] * inv, o[1][i] * inv);
-        v.y = pack_bf16_rne(o[2][i] * inv, o[3][i] * inv);
-        v.z = pack_bf16_rne(o[4][i] * inv, o[5][i] * inv);
-        v.w = pack_bf16_rne(o[6][i] * inv, o[7][i] * inv);
-        *reinterpret_cast<u32x4_t *>(dst + 8 * i) = v;
-    }
 }
 
 // ------------------------------------------------------------ page loads
@@ -528,14 +516,23 @@ __device__ __forceinline__ void process_page(const PageRaw<MIXED> &c, const Page
 
 // ------------------------------------------------------------------ kernel
 
-// LDS bytes of the wave merge: WAVES - 1 slots of accumulators, then their
-// (max, sum) per head.
+// LDS bytes of the wave merge: one slot of accumulators per wave, then their
+// (max, sum) per head, then the ticket flag.
 constexpr int kMergeSlotBytes = 8 * 64 * 16;     // one wave's accumulators: 8 x f32x4 per lane
 
 template <int WAVES>
 constexpr int merge_bytes()
 {
-    return (WAVES - 1) * (kMergeSlotBytes + 16 * 8);
+    return WAVES * (kMergeSlotBytes + 16 * 8) + 16;
+}
+
+// Write accumulator column n (channels 32G + 8i + n, i = 0..3, of one head)
+// as BF16, scaled by inv.
+__device__ __forceinline__ void store_out_col(uint16_t *dst, int n, f32x4_t c, float inv)
+{
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+        dst[8 * i + n] = (uint16_t)(pack_bf16_rne(c[i] * inv, 0.0f) & 0xFFFFu);
 }
 
 // With 8 waves per workgroup (one workgroup per CU), waves 0..3 are issued
@@ -587,7 +584,7 @@ __device__ __forceinline__ void zero_pair_output(const AttnParams &p, int b, int
 
 // One split: the tokens [s*tps, min(ctx, (s+1)*tps)) of sequence b, KV head j
 // (non-empty).  Every wave of the workgroup calls it, and every wave meets the
-// same barriers; waves other than 0 leave after the workgroup merge.
+// same barriers.
 template <bool MIXED, int WAVES>
 __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, int s, int ctx,
                                              uint8_t *sm_buf, uint32_t *sm_pt)
@@ -673,127 +670,128 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
             process_page<MIXED>(c1, i1, qB, p.scale_log2, G, st, O);
         }
     }
-    // every wave has its partial before the workgroup merge
-    __syncthreads();
-
-    // ---- merge the waves of the workgroup through LDS, as a fixed binary
-    //      tree (waves h..2h-1 hand their partial to waves 0..h-1), so every
-    //      wave takes part and the result does not depend on timing
-    float L = sum_over_groups(st.l);
-    float M = st.m;
+    // ---- merge the waves of the workgroup: every wave leaves its partial in
+    //      LDS, then wave w combines accumulator column n = w (and w + WAVES)
+    //      of all of them, in wave order, by log-sum-exp; the work is spread
+    //      over the waves and the result does not depend on timing
+    constexpr int kCols = 8 / WAVES;     // accumulator columns per wave
     f32x4_t *sm_o = reinterpret_cast<f32x4_t *>(sm_buf);
-    float2 *sm_ml = reinterpret_cast<float2 *>(sm_buf + (WAVES - 1) * kMergeSlotBytes);
+    float2 *sm_ml = reinterpret_cast<float2 *>(sm_buf + WAVES * kMergeSlotBytes);
+    int32_t *sm_flag = reinterpret_cast<int32_t *>(sm_buf + WAVES * (kMergeSlotBytes + 16 * 8));
+    {
+        const float lw = sum_over_groups(st.l);
 #pragma unroll
-    for (int h = WAVES / 2; h >= 1; h /= 2) {
-        const int slot_base = WAVES - 2 * h;     // each level has its own slots: one barrier per level
-        if (wave >= h && wave < 2 * h) {
-            const int slot = slot_base + wave - h;
+        for (int n = 0; n < 8; n++)
+            sm_o[(wave * 8 + n) * 64 + lane] = O[n];
+        if (G == 0)
+            sm_ml[wave * 16 + r] = float2{st.m, lw};
+    }
+    __syncthreads();
+    float M = -INFINITY;
+    float2 wml[WAVES];
 #pragma unroll
-            for (int n = 0; n < 8; n++)
-                sm_o[(slot * 8 + n) * 64 + lane] = O[n];
-            if (G == 0)
-                sm_ml[slot * 16 + r] = float2{M, L};
-        }
-        __syncthreads();
-        if (wave < h) {
-            const int slot = slot_base + wave;
-            const float2 ml = sm_ml[slot * 16 + r];
-            const float Mn = fmaxf(M, ml.x);
-            const float Ms = Mn == -INFINITY ? 0.0f : Mn;     // two empty partials stay empty
-            const float ca = __builtin_amdgcn_exp2f(M - Ms);
-            const float cb = __builtin_amdgcn_exp2f(ml.x - Ms);
-            L = fmaf(L, ca, ml.y * cb);
-            M = Mn;
+    for (int k = 0; k < WAVES; k++) {
+        wml[k] = sm_ml[k * 16 + r];
+        M = fmaxf(M, wml[k].x);
+    }
+    const float Ms = M == -INFINITY ? 0.0f : M;     // a head whose partials are all empty stays empty
+    float L = 0.0f;
+    f32x4_t C[kCols];
 #pragma unroll
-            for (int n = 0; n < 8; n++) {
-                const f32x4_t ob = sm_o[(slot * 8 + n) * 64 + lane];
+    for (int q = 0; q < kCols; q++)
+        C[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int i = 0; i < 4; i++)
-                    O[n][i] = fmaf(O[n][i], ca, ob[i] * cb);
-            }
+    for (int k = 0; k < WAVES; k++) {
+        const float ck = __builtin_amdgcn_exp2f(wml[k].x - Ms);
+        L = fmaf(wml[k].y, ck, L);
+#pragma unroll
+        for (int q = 0; q < kCols; q++) {
+            const f32x4_t ok = sm_o[(k * 8 + wave + q * WAVES) * 64 + lane];
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                C[q][i] = fmaf(ok[i], ck, C[q][i]);
         }
     }
-    if (wave > 0)
-        return;
+    uint16_t *orow = p.out + out_row * kHeadDim + 32 * G;
 
     if (n_split_b == 1) {
         if (head_ok) {
-            store_out_row(p.out + out_row * kHeadDim + 32 * G, O, 1.0f / L);
-            if (p.lse && G == 0)
+            const float inv = 1.0f / L;
+#pragma unroll
+            for (int q = 0; q < kCols; q++)
+                store_out_col(orow, wave + q * WAVES, C[q], inv);
+            if (p.lse && wave == 0 && G == 0)
                 p.lse[out_row] = (M + log2f(L)) * kLn2;
         }
         return;
     }
 
     // ---- several splits: publish this split's partial (device-coherent),
-    //      then the last workgroup of (b, j) to arrive merges all of them
+    //      then the last workgroup of (b, j) to arrive merges all of them.
+    //      Partial of split s: columns [8][G 4][head g] of f32x4, and
+    //      (max, sum) per head.
     const int64_t pair_id = (int64_t)b * p.hkv + j;
     const __amdgpu_buffer_rsrc_t rs_o = raw_rsrc(p.part_o + pair_id * p.n_splits * p.g * kHeadDim);
     const __amdgpu_buffer_rsrc_t rs_ml = raw_rsrc(p.part_ml + pair_id * p.n_splits * p.g);
+    auto col_offset = [&](int t, int n) { return (uint32_t)((((t * 8 + n) * 4 + G) * p.g + r) * 16); };
     if (head_ok) {
-        const uint32_t ob = (uint32_t)(((s * p.g + r) * kHeadDim + 32 * G) * 4);
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            const f32x4_t a = {O[0][i], O[1][i], O[2][i], O[3][i]};
-            const f32x4_t c = {O[4][i], O[5][i], O[6][i], O[7][i]};
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, a), rs_o, ob + 32 * i, 0,
-                                                   kCoherent);
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, c), rs_o, ob + 32 * i + 16,
-                                                   0, kCoherent);
-        }
-        if (G == 0) {
+        for (int q = 0; q < kCols; q++)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, C[q]), rs_o,
+                                                   col_offset(s, wave + q * WAVES), 0, kCoherent);
+        if (wave == 0 && G == 0) {
             const u32x2_t ml = {__float_as_uint(M), __float_as_uint(L)};
             __builtin_amdgcn_raw_buffer_store_b64(ml, rs_ml, (uint32_t)((s * p.g + r) * 8), 0, kCoherent);
         }
     }
-    // every store of this wave has completed (device-coherent) before the ticket
+    // every store of the workgroup has completed (device-coherent) before the ticket
     __builtin_amdgcn_s_waitcnt(0);
-    int last = 0;
-    if (lane == 0)
-        last = __hip_atomic_fetch_add(&p.tickets[pair_id], 1, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT) == n_split_b - 1;
-    last = __builtin_amdgcn_readfirstlane(last);
-    if (!last)
+    __syncthreads();
+    if (wave == 0) {
+        int last = 0;
+        if (lane == 0)
+            last = __hip_atomic_fetch_add(&p.tickets[pair_id], 1, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT) == n_split_b - 1;
+        if (lane == 0)
+            *sm_flag = last;
+    }
+    __syncthreads();
+    if (!__builtin_amdgcn_readfirstlane(*sm_flag))
         return;
 
     if (head_ok) {
         // online log-sum-exp fold of every split's partial, in split order
         // (the result must not depend on which workgroup arrived last); the
         // next split's device-coherent loads are in flight while one is folded
-        M = -INFINITY;
-        L = 0.0f;
+        float Mf = -INFINITY, Lf = 0.0f;
+        f32x4_t F[kCols];
 #pragma unroll
-        for (int n = 0; n < 8; n++)
-            O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        auto load_split = [&](int t, f32x4_t(&dst)[8], u32x2_t &ml) {
-            const uint32_t ob = (uint32_t)(((t * p.g + r) * kHeadDim + 32 * G) * 4);
+        for (int q = 0; q < kCols; q++)
+            F[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        auto load_split = [&](int t, f32x4_t(&dst)[kCols], u32x2_t &ml) {
 #pragma unroll
-            for (int i = 0; i < 4; i++) {
-                dst[i] = __builtin_bit_cast(
-                    f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, ob + 32 * i, 0, kCoherent));
-                dst[4 + i] = __builtin_bit_cast(
-                    f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, ob + 32 * i + 16, 0, kCoherent));
-            }
+            for (int q = 0; q < kCols; q++)
+                dst[q] = __builtin_bit_cast(
+                    f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, col_offset(t, wave + q * WAVES), 0,
+                                                                   kCoherent));
             ml = __builtin_amdgcn_raw_buffer_load_b64(rs_ml, (uint32_t)((t * p.g + r) * 8), 0, kCoherent);
         };
-        auto fold = [&](const f32x4_t(&v)[8], u32x2_t ml) {
+        auto fold = [&](const f32x4_t(&v)[kCols], u32x2_t ml) {
             const float mt = __uint_as_float(ml.x);
-            const float Mn = fmaxf(M, mt);
-            const float a = __builtin_amdgcn_exp2f(M - Mn);     // 0 for the first split
+            const float Mn = fmaxf(Mf, mt);
+            const float a = __builtin_amdgcn_exp2f(Mf - Mn);     // 0 for the first split
             const float c = __builtin_amdgcn_exp2f(mt - Mn);
-            L = fmaf(L, a, __uint_as_float(ml.y) * c);
-            M = Mn;
+            Lf = fmaf(Lf, a, __uint_as_float(ml.y) * c);
+            Mf = Mn;
 #pragma unroll
-            for (int i = 0; i < 4; i++)
+            for (int q = 0; q < kCols; q++)
 #pragma unroll
-                for (int n = 0; n < 4; n++) {
-                    O[n][i] = fmaf(O[n][i], a, v[i][n] * c);
-                    O[4 + n][i] = fmaf(O[4 + n][i], a, v[4 + i][n] * c);
-                }
+                for (int i = 0; i < 4; i++)
+                    F[q][i] = fmaf(F[q][i], a, v[q][i] * c);
         };
         // two register sets, alternating; past the end the last split is
         // re-read and not used
-        f32x4_t va[8], vb[8];
+        f32x4_t va[kCols], vb[kCols];
         u32x2_t ma, mb;
         load_split(0, va, ma);
         for (int t = 0; t < n_split_b; t += 2) {
@@ -804,11 +802,14 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
             load_split(min(t + 2, n_split_b - 1), va, ma);
             fold(vb, mb);
         }
-        store_out_row(p.out + out_row * kHeadDim + 32 * G, O, 1.0f / L);
-        if (p.lse && G == 0)
-            p.lse[out_row] = (M + log2f(L)) * kLn2;
+        const float inv = 1.0f / Lf;
+#pragma unroll
+        for (int q = 0; q < kCols; q++)
+            store_out_col(orow, wave + q * WAVES, F[q], inv);
+        if (p.lse && wave == 0 && G == 0)
+            p.lse[out_row] = (Mf + log2f(Lf)) * kLn2;
     }
-    if (lane == 0)     // ready for the next call
+    if (wave == 0 && lane == 0)     // ready for the next call
         __hip_atomic_store(&p.tickets[pair_id], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
