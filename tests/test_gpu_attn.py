@@ -270,3 +270,49 @@ def test_batch_beyond_the_schedule_tables():
     for tps in (0, 16):
         out, lse = DevKV(kv).attn(tokens_per_split=tps)
         assert_attn_close(out, lse, ref, ref_lse, what=f"B=1030 tps={tps}")
+
+
+@pytest.mark.parametrize("tps", [0, 16])
+def test_lse_is_optional(tps):
+    """lse = NULL changes nothing else: same output bits, with one split or
+    several (both workgroup shapes)."""
+    w = tiny_workload(Hq=32, Hkv=8, B=6, index=9)
+    ctx = [1, 40, 300, 511, 16, 250]
+    note(f"attn: optional lse, tps={tps}")
+    kv = make_paged(w, ctx=ctx)
+    d = DevKV(kv)
+    out_a, _ = d.attn(tokens_per_split=tps)
+    out_b, lse_b = d.attn(tokens_per_split=tps, with_lse=False)
+    assert lse_b is None
+    assert torch.equal(out_a, out_b)
+
+
+def test_concurrent_calls_on_two_streams():
+    """Calls that share no workspace may run concurrently on different
+    streams: two batches (one per workgroup shape) enqueued on two streams
+    without synchronisation in between give the bits of the same calls run
+    alone."""
+    note("attn: two streams")
+    kv1 = make_paged(tiny_workload(Hq=64, Hkv=8, B=2, index=10), ctx=[3000, 4096])
+    kv2 = make_paged(tiny_workload(Hq=16, Hkv=2, B=40, index=11),
+                     ctx=np.random.default_rng(11).integers(1, 700, 40).astype(np.int32))
+    d1, d2 = DevKV(kv1), DevKV(kv2)
+    want1, lse1 = d1.attn()
+    want2, lse2 = d2.attn(tokens_per_split=32)
+    outs = []
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for d, s, tps in ((d1, streams[0], 0), (d2, streams[1], 32)):
+        B, Hq = d.B, d.Hq
+        out = torch.full((B, Hq, 128), 0x7FC0, dtype=torch.int16, device="cuda")
+        lse = torch.full((B, Hq), float("nan"), dtype=torch.float32, device="cuda")
+        ws = hma.alloc_workspace(B, Hq, d.kv.num_kv_heads, d.max_ctx, tps)
+        torch.cuda.synchronize()
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                hma.decode_attn_bfp8(d.q, d.k_mant, d.k_exp, d.v_mant, d.v_exp, d.pt, d.ctx, d.max_ctx, out,
+                                     lse=lse, scale=d.kv.scale, num_kv_heads=d.kv.num_kv_heads,
+                                     tokens_per_split=tps, workspace=ws, stream=s)
+        outs.append((out, lse))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][0], want1) and torch.equal(outs[0][1], lse1)
+    assert torch.equal(outs[1][0], want2) and torch.equal(outs[1][1], lse2)
