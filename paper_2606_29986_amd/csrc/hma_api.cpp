@@ -17,7 +17,9 @@ constexpr int32_t kMaxGroup = 16;            // query heads per KV head (MFMA N 
 constexpr int32_t kSplitQuantum = 16;        // splits hold whole pages
 constexpr int32_t kAutoSplitQuantum = 32;
 constexpr int64_t kComputeUnits = 256;       // MI355X
-constexpr int64_t kTargetWorkgroups = 2 * kComputeUnits;   // 4-wave workgroups: two per CU
+// 4-wave workgroups: two per CU already give a CU the eight waves it needs to
+// stream at full rate (three fit and take up the splits beyond)
+constexpr int64_t kTargetWorkgroups = 2 * kComputeUnits;
 constexpr int32_t kMinAutoSplit = 256;
 constexpr int32_t kMaxAutoSplit = 2048;
 constexpr int32_t kMaxWideSplit = 8192;
@@ -42,7 +44,7 @@ int32_t splits_for(int32_t max_ctx, int32_t tps);
 // Split length for tokens_per_split = 0.  When every (sequence, KV head) pair
 // fits in one pass of one workgroup per CU, the splits are sized for exactly
 // that (8-wave workgroups); otherwise they target two 4-wave workgroups per
-// CU.
+// CU, from the longest length (the host's only length information).
 int32_t auto_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx)
 {
     const int64_t pairs = (int64_t)batch * hkv;
