@@ -237,8 +237,8 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *              set.  When NULL the HMA_PAGE_BF16 bit is ignored and every
  *              page is read from the BFP8 pools.
  *   page_table int32 [batch][max_pages_per_seq]
- *   context_lens  int32 [batch], each >= 0; a length above max_context_len
- *              is read as max_context_len
+ *   context_lens  int32 [batch]; a length above max_context_len is read as
+ *              max_context_len, a negative one as 0
  *   max_context_len  host-side bound that sizes the launch (no device read
  *              on the host); must be <= max_pages_per_seq * page_size
  *   num_q_heads % num_kv_heads == 0 and num_q_heads / num_kv_heads <= 16;

@@ -563,6 +563,13 @@ __device__ __forceinline__ WavePages wave_pages(int n_pages, int wave)
     return WavePages{first, end > first ? (end - first + 3) / 4 : 0};
 }
 
+// Context length of sequence b as the kernel uses it: clamped to the host
+// bound, and a negative length read as an empty sequence.
+__device__ __forceinline__ int context_len(const AttnParams &p, int b)
+{
+    return max(0, min(p.ctx_lens[b], p.max_ctx));
+}
+
 // Zero output (and lse = -inf) for the query heads of KV head j of an empty
 // sequence b; one wave.
 __device__ __forceinline__ void zero_pair_output(const AttnParams &p, int b, int j)
@@ -893,7 +900,7 @@ __device__ __forceinline__ bool all_lengths_equal(const AttnParams &p, int c0)
     const int lane = thread_index() & 63;
     for (int b0 = 0; b0 < p.batch; b0 += 64) {
         const int b = b0 + lane;
-        const int c = b < p.batch ? min(p.ctx_lens[b], p.max_ctx) : c0;
+        const int c = b < p.batch ? context_len(p, b) : c0;
         if (__ballot(c != c0))
             return false;
     }
@@ -920,7 +927,7 @@ __device__ __forceinline__ Plan build_plan(const AttnParams &p, int32_t *sm_ctx,
         int n_last = 0, n_long = 0;
         for (int b0 = 0; b0 < p.batch; b0 += 64) {
             const int b = b0 + lane;
-            const int c = b < p.batch ? min(p.ctx_lens[b], p.max_ctx) : 0;
+            const int c = b < p.batch ? context_len(p, b) : 0;
             const int f = c / p.tps;
             const uint64_t has_last = __ballot(c - f * p.tps > 0);
             if (b < p.batch) {
@@ -974,7 +981,7 @@ __global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void de
             __shared__ int32_t sm_level[kPlanMaxBatch];
             // equal lengths need no tables: the list is then split-major,
             // entry k = split k / batch of sequence k % batch
-            const int c0 = min(p.ctx_lens[0], p.max_ctx);
+            const int c0 = context_len(p, 0);
             const bool uniform = all_lengths_equal(p, c0);
             const int nf0 = c0 / p.tps;
             Plan plan;
@@ -1020,7 +1027,7 @@ __global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void de
     const int j = id % p.hkv;
     const int b = (id / p.hkv) % p.batch;
     const int s = id / (p.hkv * p.batch);
-    const int ctx = min(p.ctx_lens[b], p.max_ctx);
+    const int ctx = context_len(p, b);
     if (s * p.tps >= ctx) {
         // empty split; split 0 of an empty sequence owns its (zero) output
         if (s == 0 && wave == 0)

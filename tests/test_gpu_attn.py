@@ -316,3 +316,22 @@ def test_concurrent_calls_on_two_streams():
     torch.cuda.synchronize()
     assert torch.equal(outs[0][0], want1) and torch.equal(outs[0][1], lse1)
     assert torch.equal(outs[1][0], want2) and torch.equal(outs[1][1], lse2)
+
+
+@pytest.mark.parametrize("tps", [0, 16])
+def test_lengths_outside_the_bound_are_clamped(tps):
+    """A length above max_context_len is read as max_context_len and a
+    negative one as 0 (zero output, lse = -inf), on both workgroup shapes."""
+    w = tiny_workload(Hq=16, Hkv=2, B=4, index=12)
+    note(f"attn: lengths outside the bound, tps={tps}")
+    kv_in = make_paged(w, ctx=[300, 640, 5, 640])
+    kv_out = make_paged(w, ctx=[300, 640, 5, 640])
+    want, want_lse = DevKV(kv_in).attn(tokens_per_split=tps)
+    d = DevKV(kv_out)
+    d.ctx = dev(np.array([300, 5000, -7, 640], np.int32))
+    d.max_ctx = 640
+    got, got_lse = d.attn(tokens_per_split=tps)
+    for b in (0, 1, 3):
+        assert torch.equal(got[b], want[b]) and torch.equal(got_lse[b], want_lse[b])
+    assert not bf16_bits_to_f64(got[2]).any()
+    assert np.isneginf(got_lse[2].cpu().numpy()).all()
