@@ -335,3 +335,25 @@ def test_lengths_outside_the_bound_are_clamped(tps):
         assert torch.equal(got[b], want[b]) and torch.equal(got_lse[b], want_lse[b])
     assert not bf16_bits_to_f64(got[2]).any()
     assert np.isneginf(got_lse[2].cpu().numpy()).all()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_batches(seed):
+    """Random shapes against the oracle: batch 1..150, KV heads 1..8, group
+    1..16, lengths 0..600 (some empty), a random split length or the
+    library's; covers both workgroup shapes, both schedules and both
+    kernel variants."""
+    rng = np.random.default_rng(4000 + seed)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    g = int(rng.integers(1, 17))
+    B = int(rng.integers(1, 151))
+    w = tiny_workload(Hq=hkv * g, Hkv=hkv, B=B, index=20 + seed)
+    ctx = rng.integers(0, 601, B).astype(np.int32)
+    ctx[rng.random(B) < 0.1] = 0
+    tps = int(rng.choice([0, 16, 48, 128, 512]))
+    frac = float(rng.choice([0.0, 0.5]))
+    note(f"attn: random batch seed={seed} B={B} hkv={hkv} g={g} tps={tps} bf16={frac} max ctx {ctx.max()}")
+    kv = make_paged(w, ctx=ctx, bf16_fraction=frac)
+    ref, ref_lse = kv.oracle_attn()
+    out, lse = DevKV(kv).attn(tokens_per_split=tps)
+    assert_attn_close(out, lse, ref, ref_lse, what=f"random batch {seed}")
