@@ -25,6 +25,7 @@ each launch.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import math
@@ -260,6 +261,8 @@ def main():
                          "stream (hma_ingress_rebuild, one call per layer)")
     ap.add_argument("--resident-layers", type=int, default=0,
                     help="layers kept resident (0 = all that the workload defines, 8 for the trace mix)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="override the batch of a uniform-length workload (capacity comparisons)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -273,6 +276,11 @@ def main():
     import paper_2606_29986_amd as hma
 
     w = wl.WORKLOADS[args.workload]
+    if args.batch:
+        if w.ctx[0] != "uniform":
+            print(json.dumps({"error": "--batch applies to the uniform-length workloads"}))
+            sys.exit(2)
+        w = dataclasses.replace(w, batch=args.batch, name="%s-batch%d" % (w.name, args.batch))
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     ctx = wl.context_lens(w)
