@@ -5,10 +5,13 @@
 // exponent bytes are streamed from HBM once, decoded to exact BF16 in
 // registers on the VALU, and fed to the matrix cores.
 //
-// Work decomposition.  One workgroup (4 waves) owns one (sequence b, KV head
-// j, split s): the tokens [s*tps, min(ctx_b, (s+1)*tps)).  The split's slice
-// of the page table is staged in LDS once.  A wave walks the split one
-// 16-token page at a time, page c going to wave c % 4.  A page's bytes are
+// Work decomposition.  A workgroup of 8 waves (one per CU, when every split
+// fits in one pass over the CUs) or 4 waves (three per CU) handles one
+// (sequence b, KV head j, split s) at a time: the tokens
+// [s*tps, min(ctx_b, (s+1)*tps)).  Which workgroup takes which split is the
+// split schedule (below the kernel body).  The split's slice of the page
+// table is staged in LDS once.  A wave walks the split one 16-token page at a
+// time, every fourth page of its group's share.  A page's bytes are
 // loaded straight into registers in the lane layout of the matrix-core
 // operands (no LDS round trip: for this scattered-page access pattern plain
 // vector loads sustain a higher HBM rate than direct-to-LDS copies), and the
