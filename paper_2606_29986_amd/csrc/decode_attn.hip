@@ -76,7 +76,7 @@ struct AttnParams {
     float2 *part_ml;
     float *part_o;
     int32_t max_pages, batch, hq, hkv, g, tps, n_splits;
-    int32_t max_ctx;          // context lengths are clamped to this bound
+    int32_t max_ctx;          // context lengths are clamped to [0, max_ctx]
     int32_t planned;          // 1: length-aware persistent schedule (4-wave shape)
     int32_t key_interleaved;
     float scale_log2;
