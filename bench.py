@@ -552,6 +552,25 @@ def main():
         res["tiled_rebuild_us"] = round(float(np.median(t_us)), 1)
         res["tiled_rebuild_GBps"] = round(tiled_bytes / (float(np.median(t_us)) * 1e-6) / 1e9, 2)
         del tiled_src
+    # a plain 1 GiB device copy on the same box: the attention rate as a
+    # fraction of what a copy (read + write) reaches here
+    cp_a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    cp_a.fill_(1)
+    cp_b = torch.empty_like(cp_a)
+    cp_us = []
+    for rep in range(6):
+        c0_, c1_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            c0_.record(stream)
+            cp_b.copy_(cp_a)
+            c1_.record(stream)
+        torch.cuda.synchronize()
+        if rep:
+            cp_us.append(c0_.elapsed_time(c1_) * 1e3)
+    copy_gbps = 2 * (1 << 30) / (float(np.median(cp_us)) * 1e-6) / 1e9
+    res["copy_GBps"] = round(copy_gbps, 1)
+    res["attn_frac_copy"] = round(attn_gbps / copy_gbps, 4)
+    del cp_a, cp_b
     if args.ingress_requests and not mixed and not all_bf16:
         res["ingress"] = ingress_experiment(w, ctx, args.ingress_requests, attn_launch, resident,
                                             stream, max(args.steps, 10))
