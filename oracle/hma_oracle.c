@@ -18,9 +18,14 @@
  *     side produces BFP8 KV [Sec. 3.1]; the decode GPU never encodes.
  *   - Page reconstruction: BFP8 pages -> BF16 pages of the paged row-major KV
  *     cache [Sec. 1, Sec. 2.3 Challenge 2, Sec. 3.3].
+ *   - Tiled per-chip prefill shards -> BF16 pages (shard merge, post-rotary
+ *     key re-layout, decode) and -> raw BFP8 pages with the bytes unchanged
+ *     [Sec. 3.3]; the paper gives no tile byte order, the one used is stated
+ *     at ora_rebuild_tiled.
  *   - Single-token GQA decode attention over the paged cache, where each page
  *     is either raw BFP8 (decoded on read) or already BF16 [Sec. 3.3, Fig. 2],
- *     in float64 from the softmax-attention definition.
+ *     in float64 from the softmax-attention definition; keys may be stored in
+ *     the interleaved rotary order and are then relabelled on read.
  *   - Split-K partials over arbitrary contiguous token ranges and their
  *     log-sum-exp merge (a reformulation of the same softmax; not in the paper).
  *
