@@ -265,7 +265,7 @@ def main():
                     help="override the batch of a uniform-length workload (capacity comparisons)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "this benchmark runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
 
     if args.copy_probe_mib:
