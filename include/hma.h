@@ -30,14 +30,17 @@
  *
  * Conventions for every call:
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
- *     every buffer.  The library keeps no pointer and no global state: calls
- *     are reentrant and may run on different streams concurrently, provided
- *     they do not share a workspace.
+ *     every buffer.  The library keeps no pointer to caller memory.  Its only
+ *     process-wide state is a per-device cache of the attention kernel's
+ *     occupancy (queried on first use).  Calls are reentrant and may run on
+ *     different streams concurrently, provided they do not share a workspace.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream).
  *     No call synchronises or allocates.
  *   - Arguments are validated on the host before any HIP call; a rejected
  *     call enqueues nothing.  Device-resident contents (page ids in range)
- *     are the caller's contract; breaking it is undefined behaviour.
+ *     are the caller's contract; breaking it is undefined behaviour.  A
+ *     caller that wants them checked runs hma_validate_page_table on host
+ *     copies first (there is no device-side trap).
  *   - Return value: HMA_OK, or a negative hma_status.  HMA_EHIP means the
  *     launch itself failed.
  */
@@ -95,8 +98,11 @@ enum hma_status {
  *   n_pools    number of pools (>= 1 unless n_pages == 0)
  *   num_kv_heads >= 1, head_dim == 128, page_size == 16
  * Errors: HMA_EINVAL (NULL pool pointer with n_pages > 0, negative count,
- * misalignment, pool stride below 1 with n_pools > 1),
- * HMA_EUNSUPPORTED (head_dim / page_size), HMA_EHIP.
+ * misalignment, pool stride below 1 with n_pools > 1, or a destination that
+ * overlaps a source stream over the span the host can bound: pools
+ * 0 .. n_pools - 1 at their strides with n_pages pages each, the pages an
+ * identity page list touches), HMA_EUNSUPPORTED (head_dim / page_size),
+ * HMA_EHIP.
  */
 HMA_API int hma_bfp8_dequant_pages(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *dst_bf16,
                            const int32_t *src_pages, const int32_t *dst_pages, int32_t n_pages,
@@ -220,15 +226,33 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *   lse[b][h] = log(sum_t exp(s_t))              (natural log, float32)
  * k_t and v_t are the exact values of the stored BFP8 elements (or the stored
  * BF16 values of tagged pages).  Products and sums use float32; the context
- * is split into ranges of tokens_per_split tokens handled by separate
- * workgroups whose partial (max, sum, weighted values) are merged exactly by
- * log-sum-exp.  When the splits outnumber what the chip runs at once, the
- * kernel orders them itself from the device-resident lengths (full splits
- * level by level, then the shorter last splits), so a ragged batch needs no
- * host-side length information; the order does not change the result.
+ * is split into ranges handled by separate workgroups whose partial (max,
+ * sum, weighted values) are merged exactly by log-sum-exp:
+ *   - with tokens_per_split > 0, ranges of tokens_per_split tokens; when they
+ *     outnumber what the chip runs at once, the kernel orders them itself
+ *     from the device-resident lengths (full splits level by level, then the
+ *     shorter last splits);
+ *   - with tokens_per_split = 0, when the batch needs more workgroups than
+ *     one per compute unit (4-wave shape), the kernel cuts the pages of the
+ *     whole batch, per KV head and in sequence order, into equal chunks, one
+ *     per resident workgroup, built on the device from the lengths; a chunk
+ *     that spans several sequences yields one range per sequence.  Ragged
+ *     batches therefore load every compute unit equally.  Otherwise the
+ *     ranges are tokens_per_split tokens of the library's choice.
+ * A ragged batch needs no host-side length information, and the schedule
+ * depends only on the lengths: repeated calls give the same bits.
  * context_lens[b] == 0 gives out = 0 and lse = -inf.  Slots at
  * or past the context end in the last page are never used, whatever they
  * hold.
+ *
+ * Non-finite and extreme inputs: an element with E = 255 and m >= 64 is an
+ * infinity.  Attention over a context holding an infinite K or V element is
+ * outside this function's contract: the query heads that read it get
+ * non-finite results (NaN or +-Inf), where float64 arithmetic would give
+ * +-Inf or NaN by its own rules.  Finite elements of every exponent are
+ * decoded exactly; scores and sums are float32, so a score beyond the
+ * float32 range (|s_t| > ~3.4e38, possible only for block exponents near
+ * 254 with large queries) overflows as float32 does.
  *
  *   q          uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
  *   k_mant, v_mant  uint8 mantissa pools, 16-byte aligned
@@ -250,7 +274,7 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *              stored channel 2i is key channel i and 2i+1 is 64 + i (the
  *              paper's post-RoPE key re-layout, Sec. 3.3, absorbed by
  *              permuting the query once instead of the keys)
- *   tokens_per_split  0 = chosen by the library (see
+ *   tokens_per_split  0 = chosen by the library (see above and
  *              hma_decode_attn_tokens_per_split); else a positive multiple
  *              of page_size (16), at most 16384
  *   out        uint16 BF16 [batch][num_q_heads][128], 16-byte aligned
@@ -258,8 +282,15 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *   workspace  device buffer of at least hma_decode_attn_workspace_bytes()
  *              bytes for the same (batch, heads, max_context_len,
  *              tokens_per_split), 256-byte aligned, zero-filled once by the
- *              caller when allocated; every call leaves it ready for the
- *              next one.  May be NULL when the required size is 0.
+ *              caller when allocated.  Its first bytes hold one split-merge
+ *              counter per (sequence, KV head) (4 bytes each, the region
+ *              padded to 256 bytes) and the partial results follow.  Every
+ *              call leaves its counters at zero, so the buffer serves later
+ *              calls with the same batch * num_kv_heads without a new zero
+ *              fill; a call with another batch * num_kv_heads needs a buffer
+ *              zero-filled for it (its counters would otherwise land on
+ *              earlier partials).  May be NULL when the required size is 0.
+ * The argument order (key_order before tokens_per_split) is this library's.
  * Errors: HMA_EINVAL, HMA_EUNSUPPORTED, HMA_EWORKSPACE, HMA_EHIP.
  */
 HMA_API int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
@@ -274,7 +305,10 @@ HMA_API int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const
 
 /*
  * Split length the library uses for tokens_per_split = 0 (host only, no HIP
- * call).  Returns a positive multiple of 16, or 0 on invalid sizes.
+ * call).  Returns a positive multiple of 16, or 0 on invalid sizes.  It
+ * decides the workgroup shape; in the 4-wave shape the ranges come from the
+ * page-balanced chunking instead.  It assumes the 256 compute units of an
+ * MI355X (the library is built for gfx950 only).
  */
 HMA_API int32_t hma_decode_attn_tokens_per_split(int32_t batch, int32_t num_q_heads,
                                          int32_t num_kv_heads, int32_t max_context_len);
@@ -282,11 +316,37 @@ HMA_API int32_t hma_decode_attn_tokens_per_split(int32_t batch, int32_t num_q_he
 /*
  * Workspace bytes hma_decode_attn_bfp8 needs for these sizes (host only).
  * tokens_per_split = 0 means the library's choice.  Returns 0 when no
- * workspace is needed (every sequence fits one split) and (size_t)-1 on
- * invalid sizes.
+ * workspace is needed (every sequence is handled in one range) and
+ * (size_t)-1 on invalid sizes.
  */
 HMA_API size_t hma_decode_attn_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                        int32_t max_context_len, int32_t tokens_per_split);
+
+/*
+ * hma_validate_page_table -- host-side check of what hma_decode_attn_bfp8
+ * leaves to the caller (device-resident page ids in range), on HOST copies
+ * of the page table and the context lengths, for callers that want the check
+ * (debug builds, tests); the attention call itself never traps.
+ *
+ * For every sequence b, the entries the attention kernel reads -- the first
+ * ceil(min(max(context_lens[b], 0), max_context_len) / page_size) of row b --
+ * must be non-negative and name a page in range: an entry tagged
+ * HMA_PAGE_BF16 an id below num_bf16_pages, any other an id below
+ * num_bfp8_pages.  num_bf16_pages < 0 means the call passes no BF16 pools:
+ * the tag is then ignored (as the attention kernel ignores it) and every id
+ * is checked against num_bfp8_pages.
+ *
+ *   page_table   host int32 [batch][max_pages_per_seq]
+ *   context_lens host int32 [batch]
+ *   first_bad    out: flat index b * max_pages_per_seq + i of the first bad
+ *                entry, or -1 (may be NULL)
+ * Returns HMA_OK, HMA_EINVAL (a bad entry, NULL arrays with batch > 0, or
+ * bad sizes) or HMA_EUNSUPPORTED (page_size != 16).
+ */
+HMA_API int hma_validate_page_table(const int32_t *page_table, int32_t batch, int32_t max_pages_per_seq,
+                                    const int32_t *context_lens, int32_t max_context_len,
+                                    int64_t num_bfp8_pages, int64_t num_bf16_pages, int32_t page_size,
+                                    int64_t *first_bad);
 
 /* Static, never-NULL description of a status code. */
 HMA_API const char *hma_status_string(int status);

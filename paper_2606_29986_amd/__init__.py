@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
     L.hma_decode_attn_tokens_per_split.restype = i32
     L.hma_decode_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
     L.hma_decode_attn_workspace_bytes.restype = sz
+    L.hma_validate_page_table.argtypes = [vp, i32, i32, vp, i32, i64, i64, i32, vp]
+    L.hma_validate_page_table.restype = ctypes.c_int
     L.hma_status_string.argtypes = [ctypes.c_int]
     L.hma_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -123,6 +125,28 @@ def alloc_workspace(batch, num_q_heads, num_kv_heads, max_context_len, tokens_pe
     if n == 0:
         return None
     return torch.zeros(n, dtype=torch.uint8, device=device)
+
+
+def validate_page_table(page_table, context_lens, max_context_len, num_bfp8_pages, num_bf16_pages=-1,
+                        page_size=PAGE_SIZE) -> int:
+    """hma_validate_page_table on host (numpy) copies: returns -1 when every
+    entry the attention kernel would read is in range, else the flat index
+    (b * max_pages_per_seq + i) of the first bad entry.  num_bf16_pages < 0:
+    no BF16 pools (the tag bit is ignored)."""
+    import numpy as np
+    pt = np.ascontiguousarray(page_table, dtype=np.int32)
+    ctx = np.ascontiguousarray(context_lens, dtype=np.int32)
+    if pt.ndim != 2 or ctx.ndim != 1 or ctx.shape[0] != pt.shape[0]:
+        raise ValueError("page_table is [batch][max_pages], context_lens [batch]")
+    bad = ctypes.c_int64(-2)
+    rc = lib().hma_validate_page_table(pt.ctypes.data, pt.shape[0], pt.shape[1], ctx.ctypes.data,
+                                       int(max_context_len), int(num_bfp8_pages), int(num_bf16_pages),
+                                       int(page_size), ctypes.byref(bad))
+    if rc == HMA_OK:
+        return -1
+    if rc == HMA_EINVAL and bad.value >= 0:
+        return int(bad.value)
+    raise HmaError(rc, "hma_validate_page_table")
 
 
 def bfp8_dequant_pages(src_mant, src_exp, dst_bf16, src_pages, dst_pages, n_pools=1,

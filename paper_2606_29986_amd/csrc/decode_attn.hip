@@ -77,9 +77,22 @@ struct AttnParams {
     float *part_o;
     int32_t max_pages, batch, hq, hkv, g, tps, n_splits;
     int32_t max_ctx;          // context lengths are clamped to [0, max_ctx]
-    int32_t planned;          // 1: length-aware persistent schedule (4-wave shape)
+    int32_t planned;          // 1: persistent schedule built on the device (4-wave shape)
+    int32_t balanced;         // with planned: page-balanced chunks instead of tps-token splits
+    int32_t slots_per_head;   // balanced: partial slots per KV head
     int32_t key_interleaved;
     float scale_log2;
+};
+
+// One contiguous token range [t_begin, t_begin + n_tok) of (sequence b, KV
+// head j) and where its partial goes: the partials of (b, j) occupy slots
+// base .. base + n_parts - 1 of the partial arrays, this range's is slot
+// base + idx.  n_parts == 1: the range is the whole context and its result
+// is the output (no partial, no ticket).
+struct Piece {
+    int t_begin, n_tok;
+    int idx, n_parts;
+    int64_t base;
 };
 
 typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
@@ -592,11 +605,10 @@ __device__ __forceinline__ void zero_pair_output(const AttnParams &p, int b, int
         p.lse[out_row] = -INFINITY;
 }
 
-// One split: the tokens [s*tps, min(ctx, (s+1)*tps)) of sequence b, KV head j
-// (non-empty).  Every wave of the workgroup calls it, and every wave meets the
-// same barriers.
+// One piece of (sequence b, KV head j) (non-empty).  Every wave of the
+// workgroup calls it, and every wave meets the same barriers.
 template <bool MIXED, int WAVES>
-__device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, int s, int ctx,
+__device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, const Piece &pc,
                                              uint8_t *sm_buf, uint32_t *sm_pt)
 {
     const int tid = thread_index();
@@ -609,9 +621,9 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
     const int head = j * p.g + (head_ok ? r : 0);
     const int64_t out_row = (int64_t)b * p.hq + head;
 
-    const int t_begin = s * p.tps;
-    const int n_tok = min(ctx, t_begin + p.tps) - t_begin;
-    const int n_split_b = (ctx + p.tps - 1) / p.tps;
+    const int t_begin = pc.t_begin;
+    const int n_tok = pc.n_tok;
+    const int n_parts = pc.n_parts;
     const int n_pages = (n_tok + kPageSize - 1) / kPageSize;
 
     // stage this split's page-table slice in LDS
@@ -724,7 +736,7 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
     }
     uint16_t *orow = p.out + out_row * kHeadDim + 32 * G;
 
-    if (n_split_b == 1) {
+    if (n_parts == 1) {
         if (head_ok) {
             const float inv = 1.0f / L;
 #pragma unroll
@@ -736,13 +748,14 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
         return;
     }
 
-    // ---- several splits: publish this split's partial (device-coherent),
+    // ---- several pieces: publish this piece's partial (device-coherent),
     //      then the last workgroup of (b, j) to arrive merges all of them.
-    //      Partial of split s: columns [8][G 4][head g] of f32x4, and
+    //      Partial of piece t: columns [8][G 4][head g] of f32x4, and
     //      (max, sum) per head.
+    const int s = pc.idx;
     const int64_t pair_id = (int64_t)b * p.hkv + j;
-    const __amdgpu_buffer_rsrc_t rs_o = raw_rsrc(p.part_o + pair_id * p.n_splits * p.g * kHeadDim);
-    const __amdgpu_buffer_rsrc_t rs_ml = raw_rsrc(p.part_ml + pair_id * p.n_splits * p.g);
+    const __amdgpu_buffer_rsrc_t rs_o = raw_rsrc(p.part_o + pc.base * p.g * kHeadDim);
+    const __amdgpu_buffer_rsrc_t rs_ml = raw_rsrc(p.part_ml + pc.base * p.g);
     auto col_offset = [&](int t, int n) { return (uint32_t)((((t * 8 + n) * 4 + G) * p.g + r) * 16); };
     if (head_ok) {
 #pragma unroll
@@ -761,7 +774,7 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
         int last = 0;
         if (lane == 0)
             last = __hip_atomic_fetch_add(&p.tickets[pair_id], 1, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT) == n_split_b - 1;
+                                          __HIP_MEMORY_SCOPE_AGENT) == n_parts - 1;
         if (lane == 0)
             *sm_flag = last;
     }
@@ -770,9 +783,9 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
         return;
 
     if (head_ok) {
-        // online log-sum-exp fold of every split's partial, in split order
+        // online log-sum-exp fold of every piece's partial, in piece order
         // (the result must not depend on which workgroup arrived last); the
-        // next split's device-coherent loads are in flight while one is folded
+        // next piece's device-coherent loads are in flight while one is folded
         float Mf = -INFINITY, Lf = 0.0f;
         f32x4_t F[kCols];
 #pragma unroll
@@ -799,17 +812,17 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
                 for (int i = 0; i < 4; i++)
                     F[q][i] = fmaf(F[q][i], a, v[q][i] * c);
         };
-        // two register sets, alternating; past the end the last split is
+        // two register sets, alternating; past the end the last piece is
         // re-read and not used
         f32x4_t va[kCols], vb[kCols];
         u32x2_t ma, mb;
         load_split(0, va, ma);
-        for (int t = 0; t < n_split_b; t += 2) {
-            load_split(min(t + 1, n_split_b - 1), vb, mb);
+        for (int t = 0; t < n_parts; t += 2) {
+            load_split(min(t + 1, n_parts - 1), vb, mb);
             fold(va, ma);
-            if (t + 1 >= n_split_b)
+            if (t + 1 >= n_parts)
                 break;
-            load_split(min(t + 2, n_split_b - 1), va, ma);
+            load_split(min(t + 2, n_parts - 1), va, ma);
             fold(vb, mb);
         }
         const float inv = 1.0f / Lf;
@@ -821,6 +834,19 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
     }
     if (wave == 0 && lane == 0)     // ready for the next call
         __hip_atomic_store(&p.tickets[pair_id], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Split s of (b, j) under tokens_per_split splits: tokens [s*tps, min(ctx,
+// (s+1)*tps)); its partial is slot s of the pair's n_splits slots.
+__device__ __forceinline__ Piece split_piece(const AttnParams &p, int b, int j, int s, int ctx)
+{
+    Piece pc;
+    pc.t_begin = s * p.tps;
+    pc.n_tok = min(ctx, pc.t_begin + p.tps) - pc.t_begin;
+    pc.idx = s;
+    pc.n_parts = (ctx + p.tps - 1) / p.tps;
+    pc.base = ((int64_t)b * p.hkv + j) * p.n_splits;
+    return pc;
 }
 
 // ------------------------------------------------------- the split schedule
@@ -967,6 +993,85 @@ __device__ __forceinline__ Plan build_plan(const AttnParams &p, int32_t *sm_ctx,
     return plan;
 }
 
+// Page-balanced schedule (4-wave shape, automatic split length): the pages
+// of each KV head's sequences, taken in sequence order, form one list of T
+// pages that is cut into n_chunks chunks of C pages; item it = (chunk c, KV
+// head j) with the KV head fastest, and workgroup w takes items w, w + grid,
+// ...  With n_chunks = grid / Hkv every workgroup takes one item, so every
+// compute unit gets the same number of pages whatever the length mix.  A
+// chunk that covers parts of several sequences yields one piece per
+// sequence; the pieces of (b, j) come from chunks c_first(b) .. c_last(b),
+// and piece c of sequence b is partial slot c + b of KV head j (unique: for
+// two pieces (c, b) and (c', b') with c + b = c' + b' the chunks and
+// sequences would have to overlap in opposite orders).  The chunking depends
+// only on the lengths, so the result does not depend on timing.
+constexpr int kMinChunkPages = 16;
+
+__device__ __forceinline__ void balanced_schedule_table(const AttnParams &p, int32_t *sm_pre)
+{
+    // sm_pre[b] = pages of the sequences before b (clamped lengths), b <= batch
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        int carry = 0;
+        for (int b0 = 0; b0 < p.batch; b0 += 64) {
+            const int b = b0 + lane;
+            const int pages = b < p.batch ? (context_len(p, b) + kPageSize - 1) / kPageSize : 0;
+            const int incl = wave_inclusive_scan(pages);
+            if (b < p.batch)
+                sm_pre[b] = carry + incl - pages;
+            carry += __builtin_amdgcn_readlane(incl, 63);
+        }
+        if (lane == 0)
+            sm_pre[p.batch] = carry;
+    }
+    __syncthreads();
+}
+
+template <bool MIXED, int WAVES>
+__device__ __forceinline__ void balanced_schedule(const AttnParams &p, int32_t *sm_pre, uint8_t *sm_buf,
+                                                  uint32_t *sm_pt)
+{
+    balanced_schedule_table(p, sm_pre);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int T = __builtin_amdgcn_readfirstlane(sm_pre[p.batch]);
+    // chunk length C: one item per workgroup, at least kMinChunkPages, at
+    // most the page-table slice an LDS staging holds
+    const int n0 = max(1, (int)gridDim.x / p.hkv);
+    const int C = min(kMaxSplitPages, max(kMinChunkPages, (T + n0 - 1) / n0));
+    const int n_chunks = min((T + C - 1) / C, p.slots_per_head - p.batch);     // host bound holds it
+    // empty sequences own a zero output
+    for (int b = blockIdx.x; b < p.batch; b += gridDim.x)
+        if (__builtin_amdgcn_readfirstlane(sm_pre[b + 1] - sm_pre[b]) == 0)
+            for (int j = wave; j < p.hkv; j += WAVES)
+                zero_pair_output(p, b, j);
+    const int n_items = n_chunks * p.hkv;
+    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int c = it / p.hkv;
+        const int j = it - c * p.hkv;
+        const int g0 = c * C;
+        const int g1 = min(g0 + C, T);
+        for (int b = row_of(sm_pre, p.batch, g0); b < p.batch; b++) {
+            const int pb0 = __builtin_amdgcn_readfirstlane(sm_pre[b]);
+            const int pb1 = __builtin_amdgcn_readfirstlane(sm_pre[b + 1]);
+            if (pb0 >= g1)
+                break;
+            if (pb1 <= g0 || pb1 == pb0)
+                continue;     // an empty sequence has no piece (its zero output is written above)
+            const int lo = max(g0, pb0) - pb0;     // local pages [lo, hi)
+            const int hi = min(g1, pb1) - pb0;
+            const int c_first = pb0 / C;
+            const int c_last = (pb1 - 1) / C;
+            Piece pc;
+            pc.t_begin = lo * kPageSize;
+            pc.n_tok = min(context_len(p, b), hi * kPageSize) - pc.t_begin;
+            pc.idx = c - c_first;
+            pc.n_parts = c_last - c_first + 1;
+            pc.base = (int64_t)j * p.slots_per_head + c_first + b;
+            attend_split<MIXED, WAVES>(p, b, j, pc, sm_buf, sm_pt);
+        }
+    }
+}
+
 // Occupancy: the 4-wave pure-BFP8 kernel is built for three workgroups per CU
 // (at most 168 registers per lane); the others for two waves per SIMD.
 template <bool MIXED, int WAVES>
@@ -982,6 +1087,10 @@ __global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void de
         if (p.planned) {
             __shared__ int32_t sm_ctx[kPlanMaxBatch], sm_last[kPlanMaxBatch + 1];
             __shared__ int32_t sm_level[kPlanMaxBatch];
+            if (p.balanced) {
+                balanced_schedule<MIXED, WAVES>(p, sm_last, sm_buf, sm_pt);
+                return;
+            }
             // equal lengths need no tables: the list is then split-major,
             // entry k = split k / batch of sequence k % batch
             const int c0 = context_len(p, 0);
@@ -1020,7 +1129,7 @@ __global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void de
                     if (k >= plan.n_full)
                         s = ctx / p.tps;
                 }
-                attend_split<MIXED, WAVES>(p, b, j, s, ctx, sm_buf, sm_pt);
+                attend_split<MIXED, WAVES>(p, b, j, split_piece(p, b, j, s, ctx), sm_buf, sm_pt);
             }
             return;
         }
@@ -1037,19 +1146,7 @@ __global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void de
             zero_pair_output(p, b, j);
         return;
     }
-    attend_split<MIXED, WAVES>(p, b, j, s, ctx, sm_buf, sm_pt);
-}
-
-size_t attn_workspace_bytes(int32_t batch, int32_t hq, int32_t hkv, int32_t n_splits)
-{
-    if (n_splits <= 1)
-        return 0;
-    const size_t pairs = (size_t)batch * hkv;
-    const size_t g = (size_t)(hq / hkv);
-    const size_t tickets = (pairs * sizeof(int32_t) + 255) & ~(size_t)255;
-    const size_t ml = (pairs * n_splits * g * sizeof(float2) + 255) & ~(size_t)255;
-    const size_t o = pairs * n_splits * g * kHeadDim * sizeof(float);
-    return tickets + ml + o;
+    attend_split<MIXED, WAVES>(p, b, j, split_piece(p, b, j, s, ctx), sm_buf, sm_pt);
 }
 
 // Workgroups of the 4-wave kernel the whole chip holds at once (occupancy per
@@ -1099,21 +1196,13 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
     p.n_splits = a.n_splits;
     p.max_ctx = a.max_ctx;
     p.planned = a.planned;
+    p.balanced = a.balanced;
+    p.slots_per_head = a.slots_per_head;
     p.key_interleaved = a.key_interleaved;
     p.scale_log2 = a.scale * kLog2e;
-    p.tickets = nullptr;
-    p.part_ml = nullptr;
-    p.part_o = nullptr;
-    if (a.n_splits > 1) {
-        const size_t pairs = (size_t)a.batch * a.hkv;
-        const size_t g = (size_t)p.g;
-        char *ws = static_cast<char *>(a.workspace);
-        const size_t tickets = (pairs * sizeof(int32_t) + 255) & ~(size_t)255;
-        const size_t ml = (pairs * a.n_splits * g * sizeof(float2) + 255) & ~(size_t)255;
-        p.tickets = reinterpret_cast<int32_t *>(ws);
-        p.part_ml = reinterpret_cast<float2 *>(ws + tickets);
-        p.part_o = reinterpret_cast<float *>(ws + tickets + ml);
-    }
+    p.tickets = a.tickets;
+    p.part_ml = a.part_ml;
+    p.part_o = a.part_o;
     const int64_t blocks = (int64_t)a.batch * a.hkv * a.n_splits;
     const bool mixed = a.k_bf16 != nullptr && a.v_bf16 != nullptr;
     dim3 grid((unsigned)blocks);
@@ -1121,7 +1210,10 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
         const int64_t resident = resident_workgroups(mixed);
         if (resident < 1)
             return -1;
-        grid = dim3((unsigned)std::min(blocks, 2 * resident));
+        // balanced: one chunk per resident workgroup; split schedule: two
+        // rounds of the resident workgroups over the split list
+        grid = a.balanced ? dim3((unsigned)std::min<int64_t>(resident, kBalancedGridCap))
+                          : dim3((unsigned)std::min(blocks, 2 * resident));
     }
     if (a.waves == 8) {
         if (mixed)

@@ -7,6 +7,8 @@
 #include <limits.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "hma_internal.h"
 
 namespace {
@@ -24,9 +26,18 @@ constexpr int32_t kMinAutoSplit = 256;
 constexpr int32_t kMaxAutoSplit = 2048;
 constexpr int32_t kMaxWideSplit = 8192;
 
+constexpr int32_t kSupportedBlock = 16;       // channels per shared exponent
+
 bool aligned(const void *p, uintptr_t a)
 {
     return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+// [a, a + na) and [b, b + nb) share a byte
+bool overlaps(const void *a, int64_t na, const void *b, int64_t nb)
+{
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
 }
 
 int32_t round_up(int64_t x, int32_t q)
@@ -96,12 +107,22 @@ int dequant_checked(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *d
         return HMA_EINVAL;
     if (!aligned(src_mant, 16) || !aligned(src_exp, 16) || !aligned(dst_bf16, 16))
         return HMA_EINVAL;
-    if ((const void *)dst_bf16 == (const void *)src_mant || (const void *)dst_bf16 == (const void *)src_exp)
-        return HMA_EINVAL;
     if (n_pools > 1 && (src_pool_stride_pages < 1 || dst_pool_stride_pages < 1))
         return HMA_EINVAL;
     if (src_pool_stride_pages < 0 || dst_pool_stride_pages < 0)
         return HMA_EINVAL;
+    // the destination must not overlap the sources over the span the host can
+    // bound: pools 0 .. n_pools - 1 at their strides, n_pages pages each (the
+    // pages an identity page list touches; explicit lists are the caller's
+    // contract)
+    {
+        const int64_t tile = (int64_t)num_kv_heads * kSupportedPageSize * kSupportedHeadDim;
+        const int64_t sp = n_pools > 1 ? (int64_t)(n_pools - 1) * src_pool_stride_pages + n_pages : n_pages;
+        const int64_t dp = n_pools > 1 ? (int64_t)(n_pools - 1) * dst_pool_stride_pages + n_pages : n_pages;
+        if (overlaps(dst_bf16, dp * tile * 2, src_mant, sp * tile) ||
+            overlaps(dst_bf16, dp * tile * 2, src_exp, sp * tile / kSupportedBlock))
+            return HMA_EINVAL;
+    }
     const int64_t tiles = (int64_t)n_pools * n_pages * num_kv_heads;
     if (tiles / 4 + 1 > (int64_t)INT_MAX)
         return HMA_EINVAL;
@@ -117,6 +138,50 @@ int dequant_checked(const uint8_t *src_mant, const uint8_t *src_exp, uint16_t *d
                                                           src_pool_stride_pages,
                                                           dst_pool_stride_pages, num_kv_heads, s);
     return rc == 0 ? HMA_OK : HMA_EHIP;
+}
+
+// Host-side decisions of one attention call, shared by the call itself, the
+// workspace query and the no-allocation entry point.
+struct AttnPlan {
+    int32_t tps, n_splits, waves, planned, balanced, slots_per_head;
+    int64_t slots;                            // partial slots (0: no merge)
+    size_t ticket_bytes, ml_bytes, o_bytes;   // workspace regions, 256-byte multiples but the last
+};
+
+size_t align256(size_t x)
+{
+    return (x + 255) & ~(size_t)255;
+}
+
+AttnPlan attn_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx, int32_t tokens_per_split)
+{
+    AttnPlan pl;
+    const int64_t pairs = (int64_t)batch * hkv;
+    pl.tps = tokens_per_split ? tokens_per_split : auto_tokens_per_split(batch, hkv, max_ctx);
+    pl.n_splits = splits_for(max_ctx, pl.tps);
+    pl.waves = waves_for(pairs * pl.n_splits);
+    pl.planned = pl.waves == 4 && batch <= hma::kPlanMaxBatch && pl.n_splits < hma::kPlanMaxBatch;
+    // with the automatic split, the 4-wave schedule cuts the batch's pages
+    // into equal chunks on the device (ragged batches balance across CUs)
+    pl.balanced = pl.planned && tokens_per_split == 0;
+    pl.slots_per_head = 0;
+    if (pl.balanced) {
+        // chunks per KV head: at most the grid's share (one chunk per
+        // workgroup), or the count of chunks of the largest size when the
+        // pages outnumber that; piece (c, b) is slot c + b
+        const int64_t max_pages = ((int64_t)max_ctx + kSupportedPageSize - 1) / kSupportedPageSize;
+        const int64_t by_grid = (hma::kBalancedGridCap + hkv - 1) / hkv;
+        const int64_t by_size = (batch * max_pages + hma::kMaxChunkPages - 1) / hma::kMaxChunkPages;
+        pl.slots_per_head = (int32_t)(std::max(by_grid, by_size) + batch);
+        pl.slots = (int64_t)hkv * pl.slots_per_head;
+    } else {
+        pl.slots = pl.n_splits > 1 ? pairs * pl.n_splits : 0;
+    }
+    const size_t g = (size_t)(hq / hkv);
+    pl.ticket_bytes = pl.slots ? align256((size_t)pairs * sizeof(int32_t)) : 0;
+    pl.ml_bytes = pl.slots ? align256((size_t)pl.slots * g * 2 * sizeof(float)) : 0;
+    pl.o_bytes = pl.slots ? (size_t)pl.slots * g * kSupportedHeadDim * sizeof(float) : 0;
+    return pl;
 }
 
 int64_t tiled_shard_bytes(int32_t n_tokens, int32_t heads_per_shard)
@@ -151,6 +216,81 @@ int tiled_check(const uint8_t *src, int64_t src_pool_stride_bytes, int32_t n_poo
     if (units / 4 + 1 > (int64_t)INT_MAX)
         return HMA_EINVAL;
     return HMA_OK;
+}
+
+// Host-side validation of an attention call (no HIP call).
+int attn_check(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
+               const uint8_t *v_exp, const uint16_t *k_bf16, const uint16_t *v_bf16, const int32_t *page_table,
+               int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context_len, int32_t batch,
+               int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
+               int32_t key_order, int32_t tokens_per_split, const uint16_t *out, const float *lse)
+{
+    if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
+        return HMA_EINVAL;
+    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if (num_q_heads / num_kv_heads > kMaxGroup)
+        return HMA_EUNSUPPORTED;
+    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0 ||
+        tokens_per_split > hma::kMaxTokensPerSplit)
+        return HMA_EINVAL;
+    if (max_pages_per_seq < 0 || (int64_t)max_context_len > (int64_t)max_pages_per_seq * page_size)
+        return HMA_EINVAL;
+    if (!(scale == scale) || (key_order != 0 && key_order != 1))
+        return HMA_EINVAL;
+    if (batch == 0)
+        return HMA_OK;
+    if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !page_table || !context_lens || !out)
+        return HMA_EINVAL;
+    if ((k_bf16 == nullptr) != (v_bf16 == nullptr))
+        return HMA_EINVAL;
+    if (!aligned(q, 16) || !aligned(out, 16) || !aligned(k_mant, 16) || !aligned(v_mant, 16) ||
+        !aligned(k_exp, 16) || !aligned(v_exp, 16) || !aligned(k_bf16, 16) || !aligned(v_bf16, 16) ||
+        !aligned(lse, 4))
+        return HMA_EINVAL;
+    const AttnPlan pl = attn_plan(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split);
+    if ((int64_t)batch * num_kv_heads * pl.n_splits > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    return HMA_OK;
+}
+
+// Launch with the tickets at `tickets` and the partials at `partials` (NULL
+// when the plan needs none).
+int attn_launch(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
+                const uint8_t *v_exp, const uint16_t *k_bf16, const uint16_t *v_bf16, const int32_t *page_table,
+                int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context_len, int32_t batch,
+                int32_t num_q_heads, int32_t num_kv_heads, float scale, int32_t key_order, const AttnPlan &pl,
+                uint16_t *out, float *lse, uint8_t *tickets, uint8_t *partials, void *stream)
+{
+    hma::AttnLaunch a;
+    a.q = q;
+    a.k_mant = k_mant;
+    a.k_exp = k_exp;
+    a.v_mant = v_mant;
+    a.v_exp = v_exp;
+    a.k_bf16 = k_bf16;
+    a.v_bf16 = v_bf16;
+    a.page_table = page_table;
+    a.ctx_lens = context_lens;
+    a.out = out;
+    a.lse = lse;
+    a.tickets = pl.slots ? reinterpret_cast<int32_t *>(tickets) : nullptr;
+    a.part_ml = pl.slots ? reinterpret_cast<float2 *>(partials) : nullptr;
+    a.part_o = pl.slots ? reinterpret_cast<float *>(partials + pl.ml_bytes) : nullptr;
+    a.max_pages = max_pages_per_seq;
+    a.batch = batch;
+    a.hq = num_q_heads;
+    a.hkv = num_kv_heads;
+    a.tps = pl.tps;
+    a.n_splits = pl.n_splits;
+    a.max_ctx = max_context_len;
+    a.waves = pl.waves;
+    a.planned = pl.planned;
+    a.balanced = pl.balanced;
+    a.slots_per_head = pl.slots_per_head;
+    a.scale = scale;
+    a.key_interleaved = key_order;
+    return hma::launch_decode_attn(a, static_cast<hipStream_t>(stream)) == 0 ? HMA_OK : HMA_EHIP;
 }
 
 }  // namespace
@@ -224,11 +364,7 @@ int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, uint8
     const size_t exp_bytes = mant_bytes / 16;
     // the two staging buffers must not overlap each other or start at the
     // destination (the destination's extent depends on device-side page ids)
-    auto overlaps = [](const void *a, size_t na, const void *b, size_t nb) {
-        const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
-        return x < y + nb && y < x + na;
-    };
-    if (overlaps(stage_mant, mant_bytes, stage_exp, exp_bytes))
+    if (overlaps(stage_mant, (int64_t)mant_bytes, stage_exp, (int64_t)exp_bytes))
         return HMA_EINVAL;
     if ((const void *)dst_bf16 == (const void *)stage_mant || (const void *)dst_bf16 == (const void *)stage_exp)
         return HMA_EINVAL;
@@ -296,9 +432,8 @@ size_t hma_decode_attn_workspace_bytes(int32_t batch, int32_t num_q_heads, int32
     if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0 ||
         tokens_per_split > hma::kMaxTokensPerSplit)
         return (size_t)-1;
-    const int32_t tps = tokens_per_split ? tokens_per_split
-                                         : auto_tokens_per_split(batch, num_kv_heads, max_context_len);
-    return hma::attn_workspace_bytes(batch, num_q_heads, num_kv_heads, splits_for(max_context_len, tps));
+    const AttnPlan pl = attn_plan(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split);
+    return pl.ticket_bytes + pl.ml_bytes + pl.o_bytes;
 }
 
 int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
@@ -310,65 +445,57 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
                          int32_t key_order, int32_t tokens_per_split, uint16_t *out, float *lse,
                          void *workspace, size_t workspace_bytes, void *stream)
 {
-    if (!attn_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len))
-        return HMA_EINVAL;
-    if (head_dim != kSupportedHeadDim || page_size != kSupportedPageSize)
-        return HMA_EUNSUPPORTED;
-    if (num_q_heads / num_kv_heads > kMaxGroup)
-        return HMA_EUNSUPPORTED;
-    if (tokens_per_split < 0 || tokens_per_split % kSplitQuantum != 0 ||
-        tokens_per_split > hma::kMaxTokensPerSplit)
-        return HMA_EINVAL;
-    if (max_pages_per_seq < 0 || (int64_t)max_context_len > (int64_t)max_pages_per_seq * page_size)
-        return HMA_EINVAL;
-    if (!(scale == scale) || (key_order != 0 && key_order != 1))
-        return HMA_EINVAL;
-    if (batch == 0)
-        return HMA_OK;
-    if (!q || !k_mant || !k_exp || !v_mant || !v_exp || !page_table || !context_lens || !out)
-        return HMA_EINVAL;
-    if ((k_bf16 == nullptr) != (v_bf16 == nullptr))
-        return HMA_EINVAL;
-    if (!aligned(q, 16) || !aligned(out, 16) || !aligned(k_mant, 16) || !aligned(v_mant, 16) ||
-        !aligned(k_exp, 16) || !aligned(v_exp, 16) || !aligned(k_bf16, 16) || !aligned(v_bf16, 16) ||
-        !aligned(lse, 4))
-        return HMA_EINVAL;
-    const int32_t tps = tokens_per_split ? tokens_per_split
-                                         : auto_tokens_per_split(batch, num_kv_heads, max_context_len);
-    const int32_t n_splits = splits_for(max_context_len, tps);
-    if ((int64_t)batch * num_kv_heads * n_splits > (int64_t)INT_MAX)
-        return HMA_EINVAL;
-    const size_t need = hma::attn_workspace_bytes(batch, num_q_heads, num_kv_heads, n_splits);
+    const int st = attn_check(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, max_pages_per_seq,
+                              context_lens, max_context_len, batch, num_q_heads, num_kv_heads, head_dim,
+                              page_size, scale, key_order, tokens_per_split, out, lse);
+    if (st != HMA_OK || batch == 0)
+        return st;
+    const AttnPlan pl = attn_plan(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split);
+    const size_t need = pl.ticket_bytes + pl.ml_bytes + pl.o_bytes;
     if (need > 0 && (workspace == nullptr || workspace_bytes < need))
         return HMA_EWORKSPACE;
     if (need > 0 && !aligned(workspace, 256))
         return HMA_EINVAL;
+    uint8_t *ws = static_cast<uint8_t *>(workspace);
+    return attn_launch(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, max_pages_per_seq,
+                       context_lens, max_context_len, batch, num_q_heads, num_kv_heads, scale, key_order, pl,
+                       out, lse, ws, ws + pl.ticket_bytes, stream);
+}
 
-    hma::AttnLaunch a;
-    a.q = q;
-    a.k_mant = k_mant;
-    a.k_exp = k_exp;
-    a.v_mant = v_mant;
-    a.v_exp = v_exp;
-    a.k_bf16 = k_bf16;
-    a.v_bf16 = v_bf16;
-    a.page_table = page_table;
-    a.ctx_lens = context_lens;
-    a.out = out;
-    a.lse = lse;
-    a.workspace = workspace;
-    a.max_pages = max_pages_per_seq;
-    a.batch = batch;
-    a.hq = num_q_heads;
-    a.hkv = num_kv_heads;
-    a.tps = tps;
-    a.n_splits = n_splits;
-    a.max_ctx = max_context_len;
-    a.waves = waves_for((int64_t)batch * num_kv_heads * n_splits);
-    a.planned = a.waves == 4 && batch <= hma::kPlanMaxBatch && n_splits < hma::kPlanMaxBatch;
-    a.scale = scale;
-    a.key_interleaved = key_order;
-    return hma::launch_decode_attn(a, static_cast<hipStream_t>(stream)) == 0 ? HMA_OK : HMA_EHIP;
+int hma_validate_page_table(const int32_t *page_table, int32_t batch, int32_t max_pages_per_seq,
+                            const int32_t *context_lens, int32_t max_context_len, int64_t num_bfp8_pages,
+                            int64_t num_bf16_pages, int32_t page_size, int64_t *first_bad)
+{
+    if (first_bad)
+        *first_bad = -1;
+    if (batch < 0 || max_pages_per_seq < 0 || max_context_len < 0 || num_bfp8_pages < 0)
+        return HMA_EINVAL;
+    if (page_size != kSupportedPageSize)
+        return HMA_EUNSUPPORTED;
+    if ((int64_t)max_context_len > (int64_t)max_pages_per_seq * page_size)
+        return HMA_EINVAL;
+    if (batch == 0)
+        return HMA_OK;
+    if (!page_table || !context_lens)
+        return HMA_EINVAL;
+    for (int32_t b = 0; b < batch; b++) {
+        // the entries the attention kernel reads for this sequence
+        const int32_t ctx = std::min(std::max(context_lens[b], 0), max_context_len);
+        const int32_t n = (ctx + page_size - 1) / page_size;
+        for (int32_t i = 0; i < n; i++) {
+            const int64_t at = (int64_t)b * max_pages_per_seq + i;
+            const int32_t e = page_table[at];
+            const int64_t id = e & HMA_PAGE_ID_MASK;
+            const bool tagged = (e & HMA_PAGE_BF16) != 0 && num_bf16_pages >= 0;
+            const bool ok = e >= 0 && id < (tagged ? num_bf16_pages : num_bfp8_pages);
+            if (!ok) {
+                if (first_bad)
+                    *first_bad = at;
+                return HMA_EINVAL;
+            }
+        }
+    }
+    return HMA_OK;
 }
 
 }  // extern "C"

@@ -47,6 +47,12 @@ int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, ui
                            int32_t n_pools, int64_t dst_stride_pages, int32_t hkv, size_t mant_bytes,
                            size_t exp_bytes, hipStream_t stream);
 
+// Largest grid of the page-balanced schedule: it bounds the chunks per KV
+// head, hence the partial slots the host reserves.
+constexpr int32_t kBalancedGridCap = 1024;
+// Pages per chunk of the page-balanced schedule (the device clamps to these).
+constexpr int32_t kMaxChunkPages = kMaxSplitPages;
+
 struct AttnLaunch {
     const uint16_t *q;
     const uint8_t *k_mant, *k_exp, *v_mant, *v_exp;
@@ -55,20 +61,20 @@ struct AttnLaunch {
     const int32_t *ctx_lens;
     uint16_t *out;
     float *lse;
-    void *workspace;
+    int32_t *tickets;       // one per (sequence, KV head): zero before the call, left zero
+    float2 *part_ml;        // (max, sum) per partial slot and query head
+    float *part_o;          // 128 weighted values per partial slot and query head
     int32_t max_pages, batch, hq, hkv, tps, n_splits;
     int32_t max_ctx;        // host bound on the context lengths (longer ones are clamped)
     int32_t waves;          // 4 or 8 waves per workgroup
-    int32_t planned;        // length-aware persistent schedule (4 waves, batch <= kPlanMaxBatch)
+    int32_t planned;        // persistent schedule built on the device (4 waves, batch <= kPlanMaxBatch)
+    int32_t balanced;       // with planned: page-balanced chunks (automatic split length)
+    int32_t slots_per_head; // balanced: partial slots per KV head
     int32_t key_interleaved;  // K channels stored as rotary pairs (2i, 2i+1)
     float scale;
 };
 
-// Workspace layout for n_splits > 1: tickets int32 [B*Hkv] (256-byte padded),
-// then (max, sum) float2 [B*Hkv][n_splits][g], then values float
-// [B*Hkv][n_splits][g][128].
-size_t attn_workspace_bytes(int32_t batch, int32_t hq, int32_t hkv, int32_t n_splits);
-
 int launch_decode_attn(const AttnLaunch &a, hipStream_t stream);
+
 
 }  // namespace hma

@@ -29,7 +29,7 @@ def test_header_declares_the_boundary():
                             "hma_bfp8_pack_tiled", "hma_bfp8_rebuild_tiled", "hma_tiled_shard_bytes",
                             "hma_decode_attn_bfp8",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
-                            "hma_ingress_rebuild", "hma_status_string"])
+                            "hma_ingress_rebuild", "hma_status_string", "hma_validate_page_table"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -58,6 +58,19 @@ def test_split_and_workspace_queries():
     tickets = (pairs * 4 + 255) // 256 * 256
     ml = (pairs * S * g * 8 + 255) // 256 * 256
     assert ws == tickets + ml + pairs * S * g * 128 * 4
+    # the 4-wave shape with the automatic split: page-balanced chunks, whose
+    # partial slots per KV head are bounded by the grid's share of chunks
+    # (1024 / Hkv) or by the chunks of the largest size, plus one per sequence
+    B, Hkv, g, ctx = 64, 8, 5, 15192
+    assert hma.tokens_per_split(B, Hkv * g, Hkv, ctx) == 2048
+    pages = -(-ctx // 16)
+    slots = Hkv * (max(1024 // Hkv, -(-B * pages // 1024)) + B)
+    assert hma.workspace_bytes(B, Hkv * g, Hkv, ctx) == (
+        (B * Hkv * 4 + 255) // 256 * 256 + (slots * g * 8 + 255) // 256 * 256 + slots * g * 128 * 4)
+    # the same shape with an explicit split: one slot per (sequence, head, split)
+    S = -(-ctx // 2048)
+    assert hma.workspace_bytes(B, Hkv * g, Hkv, ctx, 2048) == (
+        (B * Hkv * 4 + 255) // 256 * 256 + (B * Hkv * S * g * 8 + 255) // 256 * 256 + B * Hkv * S * g * 512)
     # one split: no workspace
     assert hma.workspace_bytes(4, 32, 8, 512, 512) == 0
     assert hma.workspace_bytes(4, 32, 8, 0) == 0
@@ -100,6 +113,13 @@ def _dequant_validation(_dequant):
     for k in ("src_mant", "src_exp", "dst"):
         assert _dequant(**{k: MISALIGNED}) == hma.HMA_EINVAL, k
     assert _dequant(dst=FAKE) == hma.HMA_EINVAL           # aliases the source
+    # the span the host can bound: 4 pages of 8 x 2048 mantissa bytes from FAKE
+    assert _dequant(dst=FAKE + 4 * 8 * 2048 - 256) == hma.HMA_EINVAL   # starts inside it
+    assert _dequant(dst=FAKE - 256) == hma.HMA_EINVAL                  # ends inside it
+    assert _dequant(src_exp=FAKE * 8, dst=FAKE * 8 + 4 * 8 * 128 - 16) == hma.HMA_EINVAL
+    # two pools at a stride of 64 pages: the second pool's pages count too
+    assert _dequant(n_pools=2, src_stride=64, dst_stride=4,
+                    dst=FAKE + (64 + 3) * 8 * 2048) == hma.HMA_EINVAL
     assert _dequant(n_pools=2, src_stride=0, dst_stride=4) == hma.HMA_EINVAL
     assert _dequant(n_pools=2, src_stride=4, dst_stride=-1) == hma.HMA_EINVAL
 
@@ -225,3 +245,40 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(hma, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         hma.lib()
+
+
+def test_page_table_validator():
+    """hma_validate_page_table checks, on host copies, exactly the entries the
+    attention kernel reads: ceil(clamped length / 16) per row, ids below the
+    pool sizes, the BF16 tag checked against the BF16 pool (or ignored when
+    there is none), negative entries rejected."""
+    import numpy as np
+    B, W = 4, 8
+    pt = np.arange(B * W, dtype=np.int32).reshape(B, W)
+    ctx = np.array([0, 17, 128, 5], np.int32)
+    assert hma.validate_page_table(pt, ctx, 128, num_bfp8_pages=B * W) == -1
+    # row 1 reads 2 entries: an out-of-range third entry is never read
+    pt2 = pt.copy()
+    pt2[1, 2] = 10 ** 6
+    assert hma.validate_page_table(pt2, ctx, 128, B * W) == -1
+    pt2[1, 1] = B * W                                       # id == pool size
+    assert hma.validate_page_table(pt2, ctx, 128, B * W) == 1 * W + 1
+    pt3 = pt.copy()
+    pt3[2, 7] = -5
+    assert hma.validate_page_table(pt3, ctx, 128, B * W) == 2 * W + 7
+    # lengths are clamped to the bound, negatives read nothing
+    assert hma.validate_page_table(pt3, np.array([0, 17, 112, -3], np.int32), 112, B * W) == -1
+    assert hma.validate_page_table(pt3, np.array([0, 17, 500, -3], np.int32), 112, B * W) == -1
+    # BF16 tag: checked against the BF16 pool when one is given
+    pt4 = pt.copy()
+    pt4[3, 0] = 3 | hma.PAGE_BF16
+    assert hma.validate_page_table(pt4, ctx, 128, B * W, num_bf16_pages=4) == -1
+    assert hma.validate_page_table(pt4, ctx, 128, B * W, num_bf16_pages=3) == 3 * W
+    assert hma.validate_page_table(pt4, ctx, 128, B * W) == -1     # no BF16 pools: tag ignored
+    pt4[3, 0] = (B * W) | hma.PAGE_BF16
+    assert hma.validate_page_table(pt4, ctx, 128, B * W) == 3 * W
+    # sizes
+    with pytest.raises(hma.HmaError):
+        hma.validate_page_table(pt, ctx, 129, B * W)       # more tokens than the table holds
+    with pytest.raises(hma.HmaError):
+        hma.validate_page_table(pt, ctx, 128, B * W, page_size=32)

@@ -357,3 +357,75 @@ def test_random_batches(seed):
     ref, ref_lse = kv.oracle_attn()
     out, lse = DevKV(kv).attn(tokens_per_split=tps)
     assert_attn_close(out, lse, ref, ref_lse, what=f"random batch {seed}")
+
+
+@pytest.mark.parametrize("case", ["short_many", "mixed_lengths", "bf16_pages"])
+def test_page_balanced_schedule_pieces_span_sequences(case):
+    """The automatic split with more workgroups than one per CU cuts each KV
+    head's concatenated page list into equal chunks on the device; a chunk
+    spanning several sequences yields one piece per sequence and the pieces
+    of a (sequence, KV head) are folded in chunk order.  Many short sequences
+    (chunks of the 16-page minimum cover several of them), empty ones,
+    ragged last pages, one sequence longer than a chunk, and pages of both
+    formats: against the oracle, and bit-identical on a repeat."""
+    rng = np.random.default_rng({"short_many": 71, "mixed_lengths": 72, "bf16_pages": 73}[case])
+    if case == "short_many":
+        B, hkv, g = 300, 8, 4
+        ctx = rng.integers(0, 60, B).astype(np.int32)
+    else:
+        B, hkv, g = 90, 8, 8 if case == "mixed_lengths" else 5
+        ctx = rng.integers(1, 400, B).astype(np.int32)
+        ctx[[2, 50]] = [3000, 1500]
+    ctx[[0, 7, 8]] = [0, 0, 1]
+    w = tiny_workload(Hq=hkv * g, Hkv=hkv, B=B, index=30 + len(case))
+    assert B * hkv > 256      # the 4-wave shape, so the page-balanced schedule
+    frac = 0.5 if case == "bf16_pages" else 0.0
+    note(f"attn: page-balanced schedule, {case}: B={B} hkv={hkv} g={g} max ctx {ctx.max()} total {ctx.sum()}")
+    kv = make_paged(w, ctx=ctx, bf16_fraction=frac)
+    ref, ref_lse = kv.oracle_attn()
+    d = DevKV(kv)
+    out, lse = d.attn()
+    assert_attn_close(out, lse, ref, ref_lse, what=f"page-balanced {case}")
+    again, lse2 = d.attn()
+    assert torch.equal(out, again) and torch.equal(lse, lse2)
+
+
+def test_workspace_reuse_contract():
+    """One workspace serves repeated calls of one shape without a new zero
+    fill: every call leaves its split-merge counters at zero.  Outputs are
+    re-poisoned with NaN between the calls, so a missed merge would show.  A
+    call with a larger batch * num_kv_heads gets the buffer zero-filled again
+    first, as the header requires; a smaller one reuses it as it is."""
+    rng = np.random.default_rng(77)
+    big = make_paged(tiny_workload(Hq=64, Hkv=8, B=40, index=40),
+                     ctx=rng.integers(1, 900, 40).astype(np.int32))
+    small = make_paged(tiny_workload(Hq=64, Hkv=8, B=20, index=41),
+                       ctx=rng.integers(1, 900, 20).astype(np.int32))
+    nbytes = max(hma.workspace_bytes(40, 64, 8, int(big.ctx.max())),
+                 hma.workspace_bytes(20, 64, 8, int(small.ctx.max())))
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
+
+    def run(kv):
+        d = DevKV(kv)
+        max_ctx = d.max_ctx
+        out = torch.full((d.B, d.Hq, 128), 0x7FC0, dtype=torch.int16, device="cuda")
+        lse = torch.full((d.B, d.Hq), float("nan"), dtype=torch.float32, device="cuda")
+        hma.decode_attn_bfp8(d.q, d.k_mant, d.k_exp, d.v_mant, d.v_exp, d.pt, d.ctx, max_ctx, out, lse=lse,
+                             scale=kv.scale, num_kv_heads=8, workspace=ws)
+        torch.cuda.synchronize()
+        return out, lse
+
+    ref_s, lse_s = small.oracle_attn()
+    ref_b, lse_b = big.oracle_attn()
+    note("attn: workspace reuse, same shape twice")
+    o1, l1 = run(small)
+    o2, l2 = run(small)
+    assert_attn_close(o2, l2, ref_s, lse_s, what="second call on a reused workspace")
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    note("attn: workspace reuse, larger batch after a zero fill")
+    ws.zero_()
+    o3, l3 = run(big)
+    assert_attn_close(o3, l3, ref_b, lse_b, what="larger batch, zero-filled workspace")
+    note("attn: workspace reuse, smaller batch without a zero fill")
+    o4, l4 = run(small)
+    assert torch.equal(o4, o1) and torch.equal(l4, l1)

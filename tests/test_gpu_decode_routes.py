@@ -10,11 +10,17 @@ every exponent).  Single-token contexts make the decode observable exactly:
 * K: with ctx = 1 the log-sum-exp is the single score; a one-hot query with a
   power-of-two weight turns it into scale * q * k_0[c] computed exactly up to
   the float32 roundings of the scale, so each channel's decoded value is read
-  back through the lse.  Every exponent 0..250 with all 256 bytes.
+  back through the lse.
+
+  Every exponent 0..254 with all 256 bytes; for exponents above 252 the query
+  weight is clamped to 2^-126 (a BF16 subnormal query would be flushed by the
+  matrix cores), which keeps the score a small exact multiple of k.
 
 Reference: the oracle's decode (Sec. 3.3 reading of the format).  Exponent 255
-(infinities) is left out: the attention output over an infinite V element is
-NaN on the GPU (the low part of the split softmax weight multiplies it by 0).
+with m >= 64 (an infinity) is outside the attention call's contract (header:
+non-finite inputs give non-finite outputs); test_infinite_elements_give_non_finite_results
+checks exactly that documented behaviour, and exponent 255 with m < 64 (finite)
+is decoded exactly like the rest.
 """
 import numpy as np
 import pytest
@@ -43,7 +49,7 @@ def _kv(rng, B, Hq, sweep, half):
     v_mant = rng.integers(0, 256, (B, HKV, P, D), dtype=np.uint8)
     k_exp = np.full((B, HKV, P, D // 16), 127, np.uint8)
     v_exp = np.full((B, HKV, P, D // 16), 127, np.uint8)
-    mant, ex, cap = (v_mant, v_exp, 254) if sweep == "v" else (k_mant, k_exp, 250)
+    mant, ex, cap = (v_mant, v_exp, 254) if sweep == "v" else (k_mant, k_exp, 254)
     t = np.arange(B * HKV)
     exps = np.minimum(t % 256, cap)
     for b in range(B):
@@ -94,7 +100,7 @@ def test_k_decode_exhaustive_through_single_token_lse(mixed_kernel, B):
             ref = np.zeros((B, HKV * g))
             for b in range(B):
                 for j in range(HKV):
-                    e = 126 - int(exps[8 * b + j])
+                    e = max(126 - int(exps[8 * b + j]), -126)     # a normal BF16 weight
                     q[b, j * g + np.arange(g), chan] = (e + 127) << 7
                     ref[b, j * g: (j + 1) * g] = float(np.float32(SCALE)) * 2.0 ** e * k_dec[b, j, chan]
             d.q = torch.from_numpy(q.view(np.int16)).cuda()
@@ -104,3 +110,36 @@ def test_k_decode_exhaustive_through_single_token_lse(mixed_kernel, B):
             bad = np.argwhere(err > 1e-6 * np.abs(ref))
             assert bad.size == 0, (f"half {half} phase {phase}: {len(bad)} mismatches; first (b, h) "
                                    f"{bad[:4].tolist()} got {got[tuple(bad[0])]} ref {ref[tuple(bad[0])]}")
+
+
+@pytest.mark.parametrize("stream", ["k", "v"])
+def test_infinite_elements_give_non_finite_results(stream):
+    """Outside the contract, as documented in the header: one infinite element
+    (E = 255, m >= 64) in a sequence's K or V makes the results of the query
+    heads that read it non-finite (NaN or +-Inf) -- never a finite value that
+    hides it -- and leaves every other (sequence, KV head) exact.  Single-token
+    contexts; E = 255 with m < 64 is finite and decoded exactly."""
+    rng = np.random.default_rng(91)
+    B, g = 4, 2
+    kv, ids, _ = _kv(rng, B, HKV * g, "v", 0)
+    kv.q[:] = 0x3F80
+    mant, ex = (kv.k_mant, kv.k_exp) if stream == "k" else (kv.v_mant, kv.v_exp)
+    pid = ids[1]
+    ex[pid, 3, 0, 2] = 255          # sequence 1, KV head 3, block 2 of token 0
+    mant[pid, 3, 0, 32:48] = 5      # finite magnitudes (m < 64) ...
+    mant[pid, 3, 0, 40] = 0x40      # ... and one infinity: m = 64, sign +
+    kv.k_bf16 = oracle.decode_blocks(kv.k_mant, kv.k_exp)
+    kv.v_bf16 = oracle.decode_blocks(kv.v_mant, kv.v_exp)
+    note(f"attn: an infinite {stream} element, outside the contract")
+    out, lse = DevKV(kv).attn(use_bf16_pools=False)
+    got = oracle.bf16_to_f64(out.cpu().numpy().view(np.uint16))      # [B][Hq][D]
+    heads = [3 * g + r for r in range(g)]
+    if stream == "v":
+        assert not np.isfinite(got[1, heads, 40]).any()
+        rest = np.ones_like(got, dtype=bool)
+        rest[1, heads, 40] = False
+        assert np.isfinite(got[rest]).all()
+    else:
+        assert not np.isfinite(lse.cpu().numpy()[1, heads]).any() or not np.isfinite(got[1, heads]).all()
+        other = [h for h in range(HKV * g) if h not in heads]
+        assert np.isfinite(got[1, other]).all() and np.isfinite(got[[0, 2, 3]]).all()
