@@ -65,7 +65,8 @@ enum hma_status {
     HMA_EINVAL = -1,        /* NULL pointer, bad size, misalignment, aliasing */
     HMA_EUNSUPPORTED = -2,  /* valid but not implemented: head_dim != 128, page_size != 16, g > 16 */
     HMA_EWORKSPACE = -3,    /* workspace missing or smaller than required */
-    HMA_EHIP = -4           /* kernel launch failed */
+    HMA_EHIP = -4,          /* kernel launch failed */
+    HMA_ESCRATCH = -5       /* larger than the fixed scratch of hma_decode_attn_bfp8_noalloc */
 };
 
 #define HMA_PAGE_BF16 0x40000000     /* page-table tag: page lives in the BF16 pool */
@@ -302,6 +303,34 @@ HMA_API int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const
                          int32_t key_order,
                          int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
                          size_t workspace_bytes, void *stream);
+
+/*
+ * hma_decode_attn_bfp8_noalloc -- hma_decode_attn_bfp8 for callers that
+ * cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same arguments, validation and
+ * result, without the workspace.  The split-merge counters and partial
+ * results live in a fixed device array of HMA_NOALLOC_SCRATCH_BYTES inside
+ * the library (one per GPU, held until the process ends); the counters sit
+ * in its first 64 KiB whatever the call's shape.  The first call on a GPU
+ * clears them with a kernel on `stream`; every call leaves them at zero.
+ * Calls whose counters (4 bytes per (sequence, KV head)) exceed 64 KiB or
+ * whose partials exceed the rest of the array return HMA_ESCRATCH without
+ * launching (hma_decode_attn_workspace_bytes minus the counter region is the
+ * partials' size).  The call allocates nothing.  All calls on one GPU share
+ * its array: calls that overlap in time on one GPU (other streams, other
+ * threads) race and give undefined results -- serialize them.
+ * Errors: those of hma_decode_attn_bfp8 except HMA_EWORKSPACE, and
+ * HMA_ESCRATCH.
+ */
+#define HMA_NOALLOC_SCRATCH_BYTES (16u << 20)
+HMA_API int hma_decode_attn_bfp8_noalloc(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
+                                         const uint8_t *v_mant, const uint8_t *v_exp, const uint16_t *k_bf16,
+                                         const uint16_t *v_bf16, const int32_t *page_table,
+                                         int32_t max_pages_per_seq, const int32_t *context_lens,
+                                         int32_t max_context_len, int32_t batch, int32_t num_q_heads,
+                                         int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                                         float scale, int32_t key_order, int32_t tokens_per_split,
+                                         uint16_t *out, float *lse, void *stream);
 
 /*
  * Split length the library uses for tokens_per_split = 0 (host only, no HIP

@@ -21,6 +21,7 @@ HMA_EINVAL = -1
 HMA_EUNSUPPORTED = -2
 HMA_EWORKSPACE = -3
 HMA_EHIP = -4
+HMA_ESCRATCH = -5
 PAGE_BF16 = 0x40000000
 PAGE_ID_MASK = 0x3FFFFFFF
 HEAD_DIM = 128
@@ -61,6 +62,8 @@ def lib() -> ctypes.CDLL:
                                        i32, i32, i32, ctypes.c_float, i32, i32, vp, vp, vp, sz,
                                        vp]
     L.hma_decode_attn_bfp8.restype = ctypes.c_int
+    L.hma_decode_attn_bfp8_noalloc.argtypes = L.hma_decode_attn_bfp8.argtypes[:21] + [vp]
+    L.hma_decode_attn_bfp8_noalloc.restype = ctypes.c_int
     L.hma_decode_attn_tokens_per_split.argtypes = [i32, i32, i32, i32]
     L.hma_decode_attn_tokens_per_split.restype = i32
     L.hma_decode_attn_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
@@ -269,3 +272,23 @@ def decode_attn_bfp8(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, 
         _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_decode_attn_bfp8")
+
+
+def decode_attn_bfp8_noalloc(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len,
+                             out, k_bf16=None, v_bf16=None, lse=None, scale=None, num_kv_heads=None,
+                             tokens_per_split=0, head_dim=HEAD_DIM, page_size=PAGE_SIZE, key_order=0,
+                             stream=None) -> None:
+    """hma_decode_attn_bfp8_noalloc: decode_attn_bfp8 without a workspace (the
+    library's fixed device scratch holds the split-merge state)."""
+    _check_dev(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, out, k_bf16, v_bf16, lse)
+    B, Hq, D = q.shape
+    hkv = int(num_kv_heads if num_kv_heads is not None else k_mant.shape[1])
+    if scale is None:
+        scale = 1.0 / (D ** 0.5)
+    rc = lib().hma_decode_attn_bfp8_noalloc(
+        _ptr(q), _ptr(k_mant), _ptr(k_exp), _ptr(v_mant), _ptr(v_exp), _ptr(k_bf16),
+        _ptr(v_bf16), _ptr(page_table), int(page_table.shape[1]), _ptr(context_lens),
+        int(max_context_len), B, Hq, hkv, D, page_size, float(scale), int(key_order),
+        int(tokens_per_split), _ptr(out), _ptr(lse), _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_decode_attn_bfp8_noalloc")

@@ -47,6 +47,7 @@
 // an agent-scope fence writes back and invalidates the whole L2).
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 
 #include "hma_device.h"
 #include "hma_internal.h"
@@ -1227,6 +1228,47 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
             hipLaunchKernelGGL((decode_attn_bfp8_kernel<false, 4>), grid, dim3(256), 0, stream, p);
     }
     return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+// ------------------------------------------- scratch of the no-alloc entry
+
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+__global__ void clear_words_kernel(uint32_t *p, int n)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
+int noalloc_scratch(hipStream_t stream, uint8_t **base)
+{
+    constexpr int kMaxDevices = 64;
+    static std::atomic<uint8_t *> ptrs[kMaxDevices];
+    static std::mutex init_lock;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return -1;
+    uint8_t *ptr = ptrs[dev].load(std::memory_order_acquire);
+    if (ptr == nullptr) {
+        std::lock_guard<std::mutex> guard(init_lock);
+        ptr = ptrs[dev].load(std::memory_order_acquire);
+        if (ptr == nullptr) {
+            // the array's name is a host-side stand-in: take this device's
+            // address of it once, with the device current, and use only that
+            void *addr = nullptr;
+            if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || addr == nullptr)
+                return -1;
+            ptr = static_cast<uint8_t *>(addr);
+            // the tickets must start at zero (every call leaves its own at zero)
+            hipLaunchKernelGGL(clear_words_kernel, dim3(64), dim3(256), 0, stream,
+                               reinterpret_cast<uint32_t *>(ptr), (int)(kScratchTicketBytes / 4));
+            if (hipGetLastError() != hipSuccess)
+                return -1;
+            ptrs[dev].store(ptr, std::memory_order_release);
+        }
+    }
+    *base = ptr;
+    return 0;
 }
 
 }  // namespace hma

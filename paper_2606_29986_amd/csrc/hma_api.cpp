@@ -311,6 +311,8 @@ const char *hma_status_string(int status)
         return "workspace missing or too small";
     case HMA_EHIP:
         return "HIP launch or copy failed";
+    case HMA_ESCRATCH:
+        return "problem larger than the fixed device scratch of hma_decode_attn_bfp8_noalloc";
     default:
         return "unknown status";
     }
@@ -460,6 +462,34 @@ int hma_decode_attn_bfp8(const uint16_t *q, const uint8_t *k_mant, const uint8_t
     return attn_launch(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, max_pages_per_seq,
                        context_lens, max_context_len, batch, num_q_heads, num_kv_heads, scale, key_order, pl,
                        out, lse, ws, ws + pl.ticket_bytes, stream);
+}
+
+int hma_decode_attn_bfp8_noalloc(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
+                                 const uint8_t *v_mant, const uint8_t *v_exp, const uint16_t *k_bf16,
+                                 const uint16_t *v_bf16, const int32_t *page_table,
+                                 int32_t max_pages_per_seq, const int32_t *context_lens,
+                                 int32_t max_context_len, int32_t batch, int32_t num_q_heads,
+                                 int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
+                                 int32_t key_order, int32_t tokens_per_split, uint16_t *out, float *lse,
+                                 void *stream)
+{
+    const int st = attn_check(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, max_pages_per_seq,
+                              context_lens, max_context_len, batch, num_q_heads, num_kv_heads, head_dim,
+                              page_size, scale, key_order, tokens_per_split, out, lse);
+    if (st != HMA_OK || batch == 0)
+        return st;
+    const AttnPlan pl = attn_plan(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split);
+    // tickets sit in a fixed region of the scratch, the partials after it
+    if (pl.ticket_bytes > hma::kScratchTicketBytes ||
+        pl.ml_bytes + pl.o_bytes > hma::kScratchBytes - hma::kScratchTicketBytes)
+        return HMA_ESCRATCH;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    uint8_t *base = nullptr;
+    if (pl.slots > 0 && hma::noalloc_scratch(s, &base) != 0)
+        return HMA_EHIP;
+    return attn_launch(q, k_mant, k_exp, v_mant, v_exp, k_bf16, v_bf16, page_table, max_pages_per_seq,
+                       context_lens, max_context_len, batch, num_q_heads, num_kv_heads, scale, key_order, pl,
+                       out, lse, base, base ? base + hma::kScratchTicketBytes : nullptr, stream);
 }
 
 int hma_validate_page_table(const int32_t *page_table, int32_t batch, int32_t max_pages_per_seq,

@@ -75,6 +75,15 @@ struct AttnLaunch {
 };
 
 int launch_decode_attn(const AttnLaunch &a, hipStream_t stream);
+// Fixed device scratch of the no-allocation entry point (one per GPU, for the
+// life of the process): split-merge tickets in the first kScratchTicketBytes
+// (the same place for calls of any shape), partials after them.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr size_t kScratchTicketBytes = size_t(64) << 10;
+
+// Device address of the current device's scratch; the first call on a device
+// clears its ticket region with a kernel on `stream`.  Returns 0 or -1.
+int noalloc_scratch(hipStream_t stream, uint8_t **base);
 
 
 }  // namespace hma

@@ -27,7 +27,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == sorted(["hma_bfp8_dequant_pages", "hma_bfp8_dequant_pages_naive",
                             "hma_bfp8_pack_tiled", "hma_bfp8_rebuild_tiled", "hma_tiled_shard_bytes",
-                            "hma_decode_attn_bfp8",
+                            "hma_decode_attn_bfp8", "hma_decode_attn_bfp8_noalloc",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
                             "hma_ingress_rebuild", "hma_status_string", "hma_validate_page_table"])
 
@@ -282,3 +282,22 @@ def test_page_table_validator():
         hma.validate_page_table(pt, ctx, 129, B * W)       # more tokens than the table holds
     with pytest.raises(hma.HmaError):
         hma.validate_page_table(pt, ctx, 128, B * W, page_size=32)
+
+
+def test_noalloc_validation():
+    """hma_decode_attn_bfp8_noalloc validates like hma_decode_attn_bfp8 and
+    rejects, before any HIP call, problems larger than its fixed scratch:
+    1000 sequences x 8 KV heads x 16 query heads at 32K tokens need far more
+    than 16 MiB of partials."""
+    L = hma.lib()
+
+    def call(B=1000, Hq=128, maxctx=32768, maxp=2048, q=FAKE):
+        return L.hma_decode_attn_bfp8_noalloc(q, FAKE, FAKE, FAKE, FAKE, None, None, FAKE, maxp, FAKE, maxctx,
+                                              B, Hq, 8, 128, 16, 0.088388346, 0, 0, FAKE, None, None)
+    assert hma.workspace_bytes(1000, 128, 8, 32768) > (16 << 20)
+    assert call() == hma.HMA_ESCRATCH
+    assert "scratch" in hma.status_string(hma.HMA_ESCRATCH)
+    assert call(q=None) == hma.HMA_EINVAL
+    assert call(maxp=100) == hma.HMA_EINVAL
+    assert call(Hq=60) == hma.HMA_EINVAL
+    assert call(B=0) == hma.HMA_OK
