@@ -15,12 +15,23 @@ Prints ONE JSON line.  value = effective KV GB/s of the step: the bytes the
 method must move (BFP8 pages at 1.0625 B/element, BF16 pages at 2 B/element,
 plus Q, output and page table; for the rebuild, BFP8 read + BF16 written)
 divided by the step time.  Per-kernel figures come from HIP events recorded
-on the launch stream: the attention launches of a step run back to back
-between one event pair (average launch duration, dispatch gaps included);
+on the launch stream.  For the uniform workloads the attention launches of
+all layers are captured once in a HIP graph and each step replays it between
+one event pair (average launch duration, dispatch gaps included); the same
+launches issued one by one are timed too (attn_us_per_layer_eager).
 attn_us_p50/p99 come from a separate untimed pass with an event pair around
 each launch.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload 3]
+Beside the step the line carries, for the uniform BFP8 workloads:
+  read_ceiling  the read-only probes of libhma: the attention's BFP8 bytes
+                read in the attention's decomposition and with the heads of a
+                page read together, and a flat 1 GiB streaming read;
+  route_legs    one layer timed on codes that force the ldexp decode route,
+                on the headline's codes (packed route) under the same
+                repetition scheme, and (with the CPU baseline) on the oracle
+                encoder's codes of the workload's value distribution.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload 3] [--eager]
 """
 from __future__ import annotations
 
@@ -41,6 +52,7 @@ sys.path.insert(0, ROOT)
 import workloads as wl  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
+PAGE_ID_MASK = 0x3FFFFFFF
 KERNEL_SOURCES = ["paper_2606_29986_amd/csrc/decode_attn.hip",
                   "paper_2606_29986_amd/csrc/bfp8_dequant.hip",
                   "paper_2606_29986_amd/csrc/hma_device.h"]
@@ -85,27 +97,94 @@ def dequant_bytes(w: wl.Workload, n_pages: int, n_pools: int) -> int:
 
 # -------------------------------------------------------------- CPU baseline
 
-def cpu_baseline(w: wl.Workload, budget_s: float = 12.0):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _omp_threads(n: int) -> bool:
+    """Set the OpenMP thread count of this thread's later parallel regions
+    (the oracle's libgomp is the process's)."""
+    import ctypes
+    try:
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(n))
+        return True
+    except OSError:
+        return False
+
+
+def _time_loop(fn, budget_s: float, min_reps: int = 1):
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        fn()
+        reps += 1
+        elapsed = time.perf_counter() - t0
+        if reps >= min_reps and elapsed >= budget_s:
+            return reps, elapsed
+
+
+def cpu_baseline(w: wl.Workload, budget_s: float = 12.0, one_thread_budget_s: float = 5.0,
+                 rebuild_budget_s: float = 3.0):
     """Time the float64 oracle (as it stands) on a bounded sample of the same
-    workload: one layer of the whole batch, run repeatedly for ~budget_s."""
+    workload: one layer of the whole batch, run repeatedly for ~budget_s with
+    every host thread, then the first sequence of that layer with one thread,
+    then the oracle's page rebuild of request 0's K pages.  Returns the report
+    and the encoded layer (the oracle encoder's codes of the workload's value
+    distribution, reused by the encoded-values leg)."""
     import oracle
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     from oracle_fixtures import make_paged  # test infrastructure (value draws + encode)
     kv = make_paged(w, with_bf16_pool=False)
-    reps, elapsed = 0, 0.0
-    t0 = time.perf_counter()
-    while elapsed < budget_s:
-        oracle.decode_attn(kv.q, kv.k_mant, kv.k_exp, kv.v_mant, kv.v_exp, None, None,
-                           kv.page_table, kv.ctx, kv.num_kv_heads, kv.page_size, kv.scale)
-        reps += 1
-        elapsed = time.perf_counter() - t0
-    nbytes = reps * attn_bytes(w, kv.ctx)
     cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    return {"value": round(nbytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"float64 oracle attention over one layer of the full batch "
-                      f"({int(kv.ctx.sum())} tokens, {w.num_q_heads} heads), {reps} runs "
-                      f"in {elapsed:.1f} s; same byte accounting as the GPU figure"}
+
+    def attn(nseq):
+        oracle.decode_attn(kv.q[:nseq], kv.k_mant, kv.k_exp, kv.v_mant, kv.v_exp, None, None,
+                           kv.page_table[:nseq], kv.ctx[:nseq], kv.num_kv_heads, kv.page_size, kv.scale)
+
+    reps, elapsed = _time_loop(lambda: attn(w.batch), budget_s)
+    nbytes = reps * attn_bytes(w, kv.ctx)
+    res = {"value": round(nbytes / elapsed / 1e9, 4), "unit": "GB/s", "cores": cores,
+           "kind": "oracle",
+           "sample": f"float64 oracle attention over one layer of the full batch "
+                     f"({int(kv.ctx.sum())} tokens, {w.num_q_heads} heads), {reps} runs "
+                     f"in {elapsed:.1f} s; same byte accounting as the GPU figure",
+           "cpu_model": cpu_model()}
+    if _omp_threads(1):
+        try:
+            sub = dataclasses.replace(w, batch=1)
+            r1, e1 = _time_loop(lambda: attn(1), one_thread_budget_s)
+            res["one_thread_value"] = round(r1 * attn_bytes(sub, kv.ctx[:1]) / e1 / 1e9, 4)
+            res["one_thread_sample"] = (f"sequence 0 of the same layer ({int(kv.ctx[0])} tokens), "
+                                        f"{r1} runs in {e1:.1f} s, one OpenMP thread")
+        finally:
+            _omp_threads(cores)
+    n0 = int(wl.pages_per_seq(kv.ctx[:1], w.page_size)[0])
+    ids = kv.page_table[0, :n0] & PAGE_ID_MASK
+    km, kx = kv.k_mant[ids], kv.k_exp[ids]
+    rr, er = _time_loop(lambda: oracle.decode_blocks(km, kx), rebuild_budget_s)
+    res["rebuild_value"] = round(rr * dequant_bytes(w, n0, 1) / er / 1e9, 4)
+    res["rebuild_sample"] = (f"oracle page rebuild of request 0's K pages of one layer ({n0} pages), "
+                             f"{rr} runs in {er:.1f} s, {cores} threads; byte accounting of the "
+                             f"GPU rebuild")
+    return res, kv
+
+
+def packed_route_share(kv) -> float:
+    """Share of the (page, KV head) tiles read by the attention whose block
+    exponents all lie in 7..133 (the packed decode route)."""
+    used = np.concatenate([kv.page_table[b, :n] for b, n in
+                           enumerate(wl.pages_per_seq(kv.ctx, kv.page_size))]) & PAGE_ID_MASK
+    ok = np.ones((used.size, kv.num_kv_heads), dtype=bool)
+    for ex in (kv.k_exp, kv.v_exp):
+        e = ex[used].reshape(used.size, kv.num_kv_heads, -1)
+        ok &= ((e >= 7) & (e <= 133)).all(axis=-1)
+    return float(ok.mean())
 
 
 def copy_probe(mib: int, reps: int = 5) -> None:
@@ -242,6 +321,109 @@ def ingress_experiment(w, ctx, n_requests, attn_launch, resident, stream, steps)
 
 # --------------------------------------------------------------------- main
 
+def _time_launches(torch, stream, fn, n, warm=2):
+    """Average duration (us) of n back-to-back calls of fn(i) between one
+    event pair on `stream`."""
+    for i in range(warm):
+        fn(i)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(n):
+        fn(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / n
+
+
+def read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident, stream, attn_gbps):
+    """libhma's read-only probes on the same pools: the BFP8 bytes of one
+    attention launch read (a) in the attention's decomposition (one KV head
+    per workgroup, the same splits), (b) with the KV heads of a page read
+    together by the waves of one workgroup, and (c) a flat 1 GiB read."""
+    kv_bytes = int(wl.pages_per_seq(wl.context_lens(w), w.page_size).sum()) * w.page_size \
+        * bfp8_bytes_per_token_layer(w.num_kv_heads, w.head_dim)
+    maxp = -(-max_ctx // w.page_size)
+    out = {"bytes_per_launch": kv_bytes}
+    for name, hpw, pps in (("attn_decomposition", 1, tps // w.page_size),
+                           ("heads_together", w.num_kv_heads, None)):
+        if pps is None:                     # about one workgroup per CU
+            ns = max(1, -(-256 // w.batch))
+            pps = min(1024, -(-maxp // ns))
+        ns = -(-maxp // pps)
+        sink = torch.empty(w.batch * (w.num_kv_heads // hpw) * ns * 8, dtype=torch.int32, device=mant.device)
+
+        def probe(i, hpw=hpw, pps=pps, ns=ns, sink=sink):
+            slot = i % resident
+            hma.paged_read_probe(mant[2 * slot], expo[2 * slot], mant[2 * slot + 1], expo[2 * slot + 1],
+                                 pt_d, ctx_d, max_ctx, sink, num_kv_heads=w.num_kv_heads,
+                                 pages_per_split=pps, n_splits=ns, heads_per_workgroup=hpw, stream=stream)
+        us = _time_launches(torch, stream, probe, min(64, max(resident, 16)))
+        out[name] = {"us": round(us, 3), "GBps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
+                     "heads_per_workgroup": hpw, "pages_per_split": pps, "splits": ns}
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device=mant.device)
+    buf.fill_(3)
+    nwg = 4096
+    sink = torch.empty(nwg * 4, dtype=torch.int32, device=mant.device)
+    us = _time_launches(torch, stream, lambda i: hma.stream_read_probe(buf, sink, nwg, stream=stream), 10)
+    out["stream_1GiB"] = {"us": round(us, 1), "GBps": round((1 << 30) / (us * 1e-6) / 1e9, 1)}
+    del buf
+    out["attn_frac_of_attn_decomposition"] = round(attn_gbps / out["attn_decomposition"]["GBps"], 4)
+    return out
+
+
+def route_legs(w, hma, torch, total_pages, pt_d, ctx_d, max_ctx, q, tps, scale, stream, a_bytes):
+    """One attention layer timed on codes that force the ldexp decode route
+    (every page carries one block exponent of 134), against the headline's
+    codes (exponents 124..131: packed route), both cycling over 4 resident
+    layers so that no layer is re-read from the caches."""
+    dev = q.device
+    out = {}
+    ws = hma.alloc_workspace(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx, tps, device=dev)
+    o = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.int16, device=dev)
+    for route in ("packed", "ldexp"):
+        pools = []
+        for layer in range(4):
+            km, kx = wl.bfp8_codes_device(w, layer, "k", total_pages, dev, route=route)
+            vm, vx = wl.bfp8_codes_device(w, layer, "v", total_pages, dev, route=route)
+            pools.append((km, kx, vm, vx))
+
+        def launch(i, pools=pools):
+            km, kx, vm, vx = pools[i % 4]
+            hma.decode_attn_bfp8(q[i % q.shape[0]], km, kx, vm, vx, pt_d, ctx_d, max_ctx, o, scale=scale,
+                                 num_kv_heads=w.num_kv_heads, tokens_per_split=tps, workspace=ws,
+                                 stream=stream)
+        us = _time_launches(torch, stream, launch, 32)
+        out[route + "_route_us"] = round(us, 3)
+        out[route + "_route_GBps"] = round(a_bytes / (us * 1e-6) / 1e9, 1)
+        del pools
+    out["ldexp_over_packed"] = round(out["ldexp_route_us"] / out["packed_route_us"], 4)
+    return out
+
+
+def encoded_values_leg(w, hma, torch, kv, tps, stream, a_bytes):
+    """The layer the CPU baseline encoded (the oracle encoder's codes of the
+    workload's value distribution, outlier channels included), uploaded as 4
+    copies and timed like the route legs; with the share of its (page, KV
+    head) tiles that take the packed route."""
+    dev = torch.device("cuda", 0)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    pools = [(t(kv.k_mant), t(kv.k_exp), t(kv.v_mant), t(kv.v_exp)) for _ in range(4)]
+    qd = t(kv.q.view(np.int16))
+    ptd, cd = t(kv.page_table), t(kv.ctx)
+    max_ctx = int(kv.ctx.max())
+    ws = hma.alloc_workspace(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx, tps, device=dev)
+    o = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.int16, device=dev)
+
+    def launch(i):
+        km, kx, vm, vx = pools[i % 4]
+        hma.decode_attn_bfp8(qd, km, kx, vm, vx, ptd, cd, max_ctx, o, scale=kv.scale,
+                             num_kv_heads=w.num_kv_heads, tokens_per_split=tps, workspace=ws, stream=stream)
+    us = _time_launches(torch, stream, launch, 32)
+    return {"encoded_values_us": round(us, 3), "encoded_values_GBps": round(a_bytes / (us * 1e-6) / 1e9, 1),
+            "encoded_packed_route_share": round(packed_route_share(kv), 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -250,6 +432,10 @@ def main():
     ap.add_argument("--workload", type=int, default=3)
     ap.add_argument("--tokens-per-split", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the attention launches issued one by one (no HIP graph)")
+    ap.add_argument("--no-legs", action="store_true",
+                    help="skip the read-ceiling probes and the decode-route legs")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--kv-format", choices=["bfp8", "bf16"], default="bfp8",
@@ -353,9 +539,12 @@ def main():
         dq_pages = len(req_pages)
         bf16_dst = torch.empty((n_pools, dq_pages, w.num_kv_heads, w.page_size, w.head_dim),
                                dtype=torch.int16, device=dev)
-    tps = args.tokens_per_split or hma.tokens_per_split(w.batch, w.num_q_heads, w.num_kv_heads,
-                                                        max_ctx)
-    ws = hma.alloc_workspace(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx, tps, device=dev)
+    # the library's own choice (0) unless a split length is forced; tps is the
+    # split length that choice amounts to (the ragged batches run the
+    # page-balanced schedule instead)
+    tps_arg = args.tokens_per_split
+    tps = tps_arg or hma.tokens_per_split(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx)
+    ws = hma.alloc_workspace(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx, tps_arg, device=dev)
     scale = wl.softmax_scale(w)
     stream = torch.cuda.current_stream()
 
@@ -365,8 +554,7 @@ def main():
             expo[2 * layer_slot + 1], pt_d, ctx_d, max_ctx, out,
             k_bf16=bf16[2 * layer_slot] if (mixed or all_bf16) else None,
             v_bf16=bf16[2 * layer_slot + 1] if (mixed or all_bf16) else None,
-            scale=scale, num_kv_heads=w.num_kv_heads, tokens_per_split=tps, workspace=ws,
-            stream=stream)
+            scale=scale, num_kv_heads=w.num_kv_heads, tokens_per_split=tps_arg, workspace=ws)
 
     def dequant_launch(layer_slot=None):
         if mixed:       # this layer's fresh pages, K and V (two pools at stride total_pages)
@@ -410,12 +598,15 @@ def main():
         else:
             if record and not per_launch:
                 e0 = ev()
-            for layer in range(n_launch):
-                if per_launch:
-                    a0 = ev()
-                attn_launch(layer % resident)
-                if per_launch:
-                    evs.append(("attn", a0, ev(), 1))
+            if graph is not None and not per_launch:
+                graph.replay()
+            else:
+                for layer in range(n_launch):
+                    if per_launch:
+                        a0 = ev()
+                    attn_launch(layer % resident)
+                    if per_launch:
+                        evs.append(("attn", a0, ev(), 1))
             if record and not per_launch:
                 e1 = ev()
                 evs.append(("attn", e0, e1, n_launch))
@@ -425,9 +616,22 @@ def main():
                     evs.append(("dq", e1, ev(), 1))
         return evs
 
+    graph = None
     for _ in range(args.warmup):
         step(False)
     torch.cuda.synchronize()
+    if not mixed and not args.eager:
+        # the attention launches of all layers, captured once (they allocate
+        # nothing and clear nothing: the split counters are left at zero by
+        # every launch) and replayed by every step
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for layer in range(n_launch):
+                attn_launch(layer % resident)
+        torch.cuda.synchronize()
+        for _ in range(max(1, args.warmup)):
+            step(False)
+        torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         events.append(step(True))
@@ -440,6 +644,17 @@ def main():
             (attn_us if kind == "attn" else dq_us).append(e0.elapsed_time(e1) * 1e3 / n)
     attn_us = np.array(attn_us)
     dq_us = np.array(dq_us)
+    eager_us = None
+    if graph is not None:
+        # the same launches issued one by one (outside the timed region)
+        pairs = []
+        for _ in range(max(3, args.steps // 2)):
+            e0 = ev()
+            for layer in range(n_launch):
+                attn_launch(layer % resident)
+            pairs.append((e0, ev()))
+        torch.cuda.synchronize()
+        eager_us = float(np.mean([a.elapsed_time(b) * 1e3 / n_launch for a, b in pairs]))
     # latency distribution over single launches (outside the timed region)
     if mixed:
         single = attn_us
@@ -490,7 +705,8 @@ def main():
             "workload": w.name, "batch": w.batch, "context": "uniform %d" % max_ctx
             if w.ctx[0] == "uniform" else "ragged, max %d, total %d" % (max_ctx, int(ctx.sum())),
             "layers": w.layers, "num_q_heads": w.num_q_heads, "num_kv_heads": w.num_kv_heads,
-            "head_dim": w.head_dim, "page_size": w.page_size, "tokens_per_split": tps,
+            "head_dim": w.head_dim, "page_size": w.page_size,
+            "tokens_per_split": tps_arg if tps_arg else "automatic (%d)" % tps,
             "resident_layers": resident, "bf16_page_fraction": w.bf16_page_fraction,
             "kv_format": "bf16 (every page already BF16)" if all_bf16 else
                          ("mixed" if mixed else "bfp8"),
@@ -502,6 +718,9 @@ def main():
                      "%d layers (%d pages each)" % (n_launch, w.layers, dq_pages)),
         },
         "attn_us_per_layer": round(attn_mean, 3),
+        "attn_launch": "hip graph of the %d layer launches, replayed per step" % n_launch
+                       if graph is not None else "launched one by one",
+        "attn_us_per_layer_eager": round(eager_us, 3) if eager_us is not None else round(attn_mean, 3),
         "attn_us_p50": round(float(np.percentile(single, 50)), 3),
         "attn_us_p99": round(float(np.percentile(single, 99)), 3),
         "attn_GBps": round(attn_gbps, 2),
@@ -552,6 +771,12 @@ def main():
         res["tiled_rebuild_us"] = round(float(np.median(t_us)), 1)
         res["tiled_rebuild_GBps"] = round(tiled_bytes / (float(np.median(t_us)) * 1e-6) / 1e9, 2)
         del tiled_src
+    legs = not mixed and not all_bf16 and not args.no_legs
+    if legs:
+        res["read_ceiling"] = read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident,
+                                           stream, attn_gbps)
+        res["route_legs"] = route_legs(w, hma, torch, total_pages, pt_d, ctx_d, max_ctx, q, tps_arg, scale,
+                                       stream, a_bytes)
     # a plain 1 GiB device copy on the same box: the attention rate as a
     # fraction of what a copy (read + write) reaches here
     cp_a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -575,7 +800,10 @@ def main():
         res["ingress"] = ingress_experiment(w, ctx, args.ingress_requests, attn_launch, resident,
                                             stream, max(args.steps, 10))
     if not args.no_cpu_baseline and not all_bf16:
-        res["cpu_baseline"] = cpu_baseline(w)
+        res["cpu_baseline"], enc = cpu_baseline(w)
+        if legs:
+            res["route_legs"].update(encoded_values_leg(w, hma, torch, enc, tps_arg, stream, a_bytes))
+        del enc
     print(json.dumps(res), flush=True)
 
 

@@ -30,10 +30,12 @@
  *
  * Conventions for every call:
  *   - Pointers are DEVICE pointers unless stated otherwise; the caller owns
- *     every buffer.  The library keeps no pointer to caller memory.  Its only
+ *     every buffer.  The library keeps no pointer to caller memory.  Its
  *     process-wide state is a per-device cache of the attention kernel's
- *     occupancy (queried on first use).  Calls are reentrant and may run on
- *     different streams concurrently, provided they do not share a workspace.
+ *     occupancy (queried on first use) and the fixed device scratch of
+ *     hma_decode_attn_bfp8_noalloc with its per-device address.  Calls are
+ *     reentrant and may run on different streams concurrently, provided they
+ *     do not share a workspace (nor, for the no-allocation entry, a GPU).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = default stream).
  *     No call synchronises or allocates.
  *   - Arguments are validated on the host before any HIP call; a rejected
@@ -376,6 +378,48 @@ HMA_API int hma_validate_page_table(const int32_t *page_table, int32_t batch, in
                                     const int32_t *context_lens, int32_t max_context_len,
                                     int64_t num_bfp8_pages, int64_t num_bf16_pages, int32_t page_size,
                                     int64_t *first_bad);
+
+/*
+ * Read probes -- measurement, not part of the method: the HBM read ceiling
+ * that the fused attention of Sec. 3.3 (whose cost is its read of the BFP8
+ * pages) is compared against.  Both only read and XOR; each wave writes the
+ * XOR of every 32-bit word it loaded to `sink`, so the XOR of all sink words
+ * equals the XOR of all words of the bytes read, whatever the order.
+ *
+ * hma_paged_read_probe reads exactly the BFP8 bytes of an attention call
+ * over BFP8 pages: for every sequence b and KV head j, the K and V mantissa
+ * tiles (2048 B) and exponent tiles (128 B) of the pages named by the first
+ * ceil(min(max(context_lens[b], 0), max_context_len) / 16) entries of row b
+ * (the HMA_PAGE_BF16 tag is ignored: every entry is read as a BFP8 page).
+ * Decomposition: one workgroup of 8 waves per (sequence, group of
+ * heads_per_workgroup KV heads, split of pages_per_split pages); wave w reads
+ * head w mod heads_per_workgroup of the group and every
+ * (8 / heads_per_workgroup)-th page of the split.  heads_per_workgroup = 1 is
+ * the attention kernel's decomposition (one KV head per workgroup);
+ * heads_per_workgroup = num_kv_heads reads the heads of a page together.
+ *   sink        device uint32 [batch * (num_kv_heads / heads_per_workgroup)
+ *               * n_splits * 8]; sink_words is its length
+ * Returns HMA_EINVAL for NULL or misaligned (16 B) pools, heads_per_workgroup
+ * not in {1, 2, 4, 8} or not dividing num_kv_heads, pages_per_split outside
+ * [1, 1024], n_splits * pages_per_split * 16 < max_context_len,
+ * max_context_len > max_pages_per_seq * 16, or a short sink.
+ */
+HMA_API int hma_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
+                                 const uint8_t *v_exp, const int32_t *page_table, int32_t max_pages_per_seq,
+                                 const int32_t *context_lens, int32_t max_context_len, int32_t batch,
+                                 int32_t num_kv_heads, int32_t heads_per_workgroup, int32_t pages_per_split,
+                                 int32_t n_splits, uint32_t *sink, size_t sink_words, void *stream);
+
+/*
+ * hma_stream_read_probe reads `bytes` contiguous bytes (a positive multiple
+ * of 16, `buf` 16-byte aligned) with non-temporal 128-bit loads over
+ * n_workgroups workgroups of 4 waves (grid-stride).
+ *   sink        device uint32 [n_workgroups * 4]; sink_words is its length
+ * Returns HMA_EINVAL for a NULL or misaligned buffer, bytes not a positive
+ * multiple of 16, n_workgroups outside [1, 1048576] or a short sink.
+ */
+HMA_API int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workgroups, uint32_t *sink,
+                                  size_t sink_words, void *stream);
 
 /* Static, never-NULL description of a status code. */
 HMA_API const char *hma_status_string(int status);

@@ -70,6 +70,10 @@ def lib() -> ctypes.CDLL:
     L.hma_decode_attn_workspace_bytes.restype = sz
     L.hma_validate_page_table.argtypes = [vp, i32, i32, vp, i32, i64, i64, i32, vp]
     L.hma_validate_page_table.restype = ctypes.c_int
+    L.hma_paged_read_probe.argtypes = [vp, vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, i32, i32, vp, sz, vp]
+    L.hma_paged_read_probe.restype = ctypes.c_int
+    L.hma_stream_read_probe.argtypes = [vp, sz, i32, vp, sz, vp]
+    L.hma_stream_read_probe.restype = ctypes.c_int
     L.hma_status_string.argtypes = [ctypes.c_int]
     L.hma_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -292,3 +296,29 @@ def decode_attn_bfp8_noalloc(q, k_mant, k_exp, v_mant, v_exp, page_table, contex
         int(tokens_per_split), _ptr(out), _ptr(lse), _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_decode_attn_bfp8_noalloc")
+
+
+def paged_read_probe(k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len, sink,
+                     num_kv_heads, pages_per_split, n_splits, heads_per_workgroup=1, stream=None) -> None:
+    """hma_paged_read_probe: read (and XOR) the BFP8 bytes of an attention call
+    in its decomposition; sink is a uint32/int32 device tensor of
+    batch * (num_kv_heads / heads_per_workgroup) * n_splits * 8 words."""
+    _check_dev(k_mant, k_exp, v_mant, v_exp, page_table, context_lens, sink)
+    B = int(page_table.shape[0])
+    rc = lib().hma_paged_read_probe(
+        _ptr(k_mant), _ptr(k_exp), _ptr(v_mant), _ptr(v_exp), _ptr(page_table), int(page_table.shape[1]),
+        _ptr(context_lens), int(max_context_len), B, int(num_kv_heads), int(heads_per_workgroup),
+        int(pages_per_split), int(n_splits), _ptr(sink), int(sink.numel()), _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_paged_read_probe")
+
+
+def stream_read_probe(buf, sink, n_workgroups, stream=None) -> None:
+    """hma_stream_read_probe: read (and XOR) a contiguous device buffer;
+    sink holds n_workgroups * 4 words."""
+    _check_dev(buf, sink)
+    nbytes = int(buf.numel()) * int(buf.element_size())
+    rc = lib().hma_stream_read_probe(_ptr(buf), nbytes, int(n_workgroups), _ptr(sink), int(sink.numel()),
+                                     _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_stream_read_probe")

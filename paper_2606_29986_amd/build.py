@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libhma.so")
 
-SOURCES = ["hma_api.cpp", "bfp8_dequant.hip", "decode_attn.hip", "rebuild_tiled.hip"]
+SOURCES = ["hma_api.cpp", "bfp8_dequant.hip", "decode_attn.hip", "rebuild_tiled.hip", "read_probe.hip"]
 ARCH = "gfx950"
 
 

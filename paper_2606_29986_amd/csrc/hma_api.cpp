@@ -528,4 +528,53 @@ int hma_validate_page_table(const int32_t *page_table, int32_t batch, int32_t ma
     return HMA_OK;
 }
 
+int hma_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant, const uint8_t *v_exp,
+                         const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *context_lens,
+                         int32_t max_context_len, int32_t batch, int32_t num_kv_heads,
+                         int32_t heads_per_workgroup, int32_t pages_per_split, int32_t n_splits, uint32_t *sink,
+                         size_t sink_words, void *stream)
+{
+    if (batch < 0 || num_kv_heads <= 0 || max_pages_per_seq < 0 || max_context_len < 0)
+        return HMA_EINVAL;
+    const int32_t hpw = heads_per_workgroup;
+    if (!(hpw == 1 || hpw == 2 || hpw == 4 || hpw == 8) || num_kv_heads % hpw != 0)
+        return HMA_EINVAL;
+    if (pages_per_split < 1 || pages_per_split > hma::kMaxSplitPages || n_splits < 1)
+        return HMA_EINVAL;
+    if ((int64_t)n_splits * pages_per_split * kSupportedPageSize < max_context_len ||
+        (int64_t)max_context_len > (int64_t)max_pages_per_seq * kSupportedPageSize)
+        return HMA_EINVAL;
+    const int64_t grid = (int64_t)batch * (num_kv_heads / hpw) * n_splits;
+    if (grid > INT_MAX)
+        return HMA_EINVAL;
+    if (batch == 0)
+        return HMA_OK;
+    if (!k_mant || !k_exp || !v_mant || !v_exp || !page_table || !context_lens || !sink)
+        return HMA_EINVAL;
+    if (!aligned(k_mant, 16) || !aligned(k_exp, 16) || !aligned(v_mant, 16) || !aligned(v_exp, 16) ||
+        !aligned(page_table, 4) || !aligned(context_lens, 4) || !aligned(sink, 4))
+        return HMA_EINVAL;
+    if (sink_words < (size_t)grid * 8)
+        return HMA_EINVAL;
+    return hma::launch_paged_read_probe(k_mant, k_exp, v_mant, v_exp, page_table, max_pages_per_seq,
+                                        context_lens, max_context_len, batch, num_kv_heads, hpw,
+                                        pages_per_split, n_splits, sink, static_cast<hipStream_t>(stream)) == 0
+               ? HMA_OK
+               : HMA_EHIP;
+}
+
+int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workgroups, uint32_t *sink, size_t sink_words,
+                          void *stream)
+{
+    if (!buf || !sink || !aligned(buf, 16) || !aligned(sink, 4))
+        return HMA_EINVAL;
+    if (bytes == 0 || bytes % 16 != 0 || n_workgroups < 1 || n_workgroups > (1 << 20))
+        return HMA_EINVAL;
+    if (sink_words < (size_t)n_workgroups * 4)
+        return HMA_EINVAL;
+    return hma::launch_stream_read_probe(buf, bytes, sink, n_workgroups, static_cast<hipStream_t>(stream)) == 0
+               ? HMA_OK
+               : HMA_EHIP;
+}
+
 }  // extern "C"

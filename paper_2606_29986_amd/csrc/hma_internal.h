@@ -85,5 +85,14 @@ constexpr size_t kScratchTicketBytes = size_t(64) << 10;
 // clears its ticket region with a kernel on `stream`.  Returns 0 or -1.
 int noalloc_scratch(hipStream_t stream, uint8_t **base);
 
+// Read-only probes (read_probe.hip): the attention's BFP8 bytes in its
+// decomposition, and one contiguous buffer; each wave writes an XOR to sink.
+int launch_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
+                            const uint8_t *v_exp, const int32_t *page_table, int32_t max_pages,
+                            const int32_t *ctx, int32_t max_ctx, int32_t batch, int32_t hkv,
+                            int32_t heads_per_wg, int32_t pages_per_split, int32_t n_splits, uint32_t *sink,
+                            hipStream_t stream);
+int launch_stream_read_probe(const void *buf, uint64_t bytes, uint32_t *sink, int32_t n_workgroups,
+                             hipStream_t stream);
 
 }  // namespace hma

@@ -29,7 +29,8 @@ def test_header_declares_the_boundary():
                             "hma_bfp8_pack_tiled", "hma_bfp8_rebuild_tiled", "hma_tiled_shard_bytes",
                             "hma_decode_attn_bfp8", "hma_decode_attn_bfp8_noalloc",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
-                            "hma_ingress_rebuild", "hma_status_string", "hma_validate_page_table"])
+                            "hma_ingress_rebuild", "hma_status_string", "hma_validate_page_table",
+                            "hma_paged_read_probe", "hma_stream_read_probe"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -301,3 +302,35 @@ def test_noalloc_validation():
     assert call(maxp=100) == hma.HMA_EINVAL
     assert call(Hq=60) == hma.HMA_EINVAL
     assert call(B=0) == hma.HMA_OK
+
+
+def test_read_probe_validation():
+    """The read probes reject bad shapes, pools and sinks before any HIP call."""
+    L = hma.lib()
+
+    def paged(B=4, maxp=64, maxctx=1000, hkv=8, hpw=1, pps=32, ns=2, sink_words=None, k=FAKE, pt=FAKE):
+        words = B * (hkv // hpw) * ns * 8 if sink_words is None else sink_words
+        return L.hma_paged_read_probe(k, FAKE, FAKE, FAKE, pt, maxp, FAKE, maxctx, B, hkv, hpw, pps, ns,
+                                      FAKE, words, None)
+    assert paged(k=None) == hma.HMA_EINVAL
+    assert paged(k=MISALIGNED) == hma.HMA_EINVAL
+    assert paged(pt=None) == hma.HMA_EINVAL
+    assert paged(hpw=3) == hma.HMA_EINVAL                 # not 1, 2, 4 or 8
+    assert paged(hkv=4, hpw=8) == hma.HMA_EINVAL          # does not divide the KV heads
+    assert paged(pps=0) == hma.HMA_EINVAL
+    assert paged(pps=1025) == hma.HMA_EINVAL              # beyond the staged page-table slice
+    assert paged(ns=1) == hma.HMA_EINVAL                  # 32 pages do not cover 1000 tokens
+    assert paged(maxctx=1025, maxp=64) == hma.HMA_EINVAL  # more tokens than the table holds
+    assert paged(sink_words=4 * 8 * 2 * 8 - 1) == hma.HMA_EINVAL
+    assert paged(B=0) == hma.HMA_OK                       # nothing to read
+
+    def stream(buf=FAKE, nbytes=1 << 20, nwg=64, sink_words=None):
+        return L.hma_stream_read_probe(buf, nbytes, nwg, FAKE, 4 * nwg if sink_words is None else sink_words,
+                                       None)
+    assert stream(buf=None) == hma.HMA_EINVAL
+    assert stream(buf=MISALIGNED) == hma.HMA_EINVAL
+    assert stream(nbytes=0) == hma.HMA_EINVAL
+    assert stream(nbytes=1000) == hma.HMA_EINVAL          # not a multiple of 16
+    assert stream(nwg=0) == hma.HMA_EINVAL
+    assert stream(nwg=(1 << 20) + 1) == hma.HMA_EINVAL
+    assert stream(sink_words=255) == hma.HMA_EINVAL

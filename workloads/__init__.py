@@ -190,15 +190,24 @@ def garbage_bytes(w: Workload, n: int, salt: int = 0) -> np.ndarray:
 
 # ----------------------------------------------- bulk device draws (bench)
 
-def bfp8_codes_device(w: Workload, layer: int, kind: str, num_pages: int, device):
+def bfp8_codes_device(w: Workload, layer: int, kind: str, num_pages: int, device, route: str = "packed"):
     """Random BFP8 byte streams drawn directly on the device (benchmark only).
 
     Mantissa bytes are uniform over all 256 sign/magnitude codes; exponent
     bytes are uniform over 124..131, the range the BF16 draws above produce.
-    The kernels have no value-dependent control flow, so timing does not
-    depend on the distribution.  Returns (mant uint8, exp uint8) tensors of
-    shapes [pages][Hkv][P][D] and [pages][Hkv][P][D/16]."""
+    The fused attention's work per page depends on the data in two places:
+    it picks one of two exact decode routes per (page, KV head) -- the packed
+    16-bit route when every block exponent of the page lies in 7..133, the
+    ldexp route otherwise -- and it skips the rescale of its accumulators
+    when a page does not raise the running maximum.  Exponents in 124..131
+    always take the packed route.  route="ldexp" forces the other one: the
+    first block exponent of token 0 of every (page, KV head) is set to 134
+    (elements up to 254, still finite).  Encoder-produced values of the
+    outlier workloads mix both routes.  Returns (mant uint8, exp uint8)
+    tensors of shapes [pages][Hkv][P][D] and [pages][Hkv][P][D/16]."""
     import torch
+    if route not in ("packed", "ldexp"):
+        raise ValueError(route)
     g = torch.Generator(device=device)
     g.manual_seed(int(np.random.SeedSequence(
         1000 + w.index, spawn_key=(_STREAMS["codes"], layer, 0 if kind == "k" else 1)
@@ -207,4 +216,6 @@ def bfp8_codes_device(w: Workload, layer: int, kind: str, num_pages: int, device
     mant = torch.randint(0, 256, shp, dtype=torch.uint8, device=device, generator=g)
     exp = torch.randint(124, 132, shp[:-1] + (w.head_dim // 16,), dtype=torch.uint8,
                         device=device, generator=g)
+    if route == "ldexp":
+        exp[:, :, 0, 0] = 134
     return mant, exp
