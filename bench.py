@@ -336,39 +336,54 @@ def _time_launches(torch, stream, fn, n, warm=2):
     return e0.elapsed_time(e1) * 1e3 / n
 
 
-def read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident, stream, attn_gbps):
-    """libhma's read-only probes on the same pools: the BFP8 bytes of one
-    attention launch read (a) in the attention's decomposition (one KV head
-    per workgroup, the same splits), (b) with the KV heads of a page read
-    together by the waves of one workgroup, and (c) a flat 1 GiB read."""
+def read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident, stream, attn_us):
+    """libhma's read-only probes: the BFP8 bytes of one attention launch read
+    as one contiguous stream (every workload), and -- for the uniform-length
+    workloads, whose attention runs the static split grid -- read from the
+    pools in the attention's decomposition (one KV head per workgroup, the
+    same splits) and with the KV heads of a page read together; plus a flat
+    1 GiB read.  attn_over_* = attention launch time / probe time over the
+    same bytes (the ragged batches run a page-balanced schedule that no
+    static grid reproduces, so they get the stream figure only)."""
     kv_bytes = int(wl.pages_per_seq(wl.context_lens(w), w.page_size).sum()) * w.page_size \
         * bfp8_bytes_per_token_layer(w.num_kv_heads, w.head_dim)
     maxp = -(-max_ctx // w.page_size)
+    dev = mant.device
     out = {"bytes_per_launch": kv_bytes}
-    for name, hpw, pps in (("attn_decomposition", 1, tps // w.page_size),
-                           ("heads_together", w.num_kv_heads, None)):
-        if pps is None:                     # about one workgroup per CU
-            ns = max(1, -(-256 // w.batch))
-            pps = min(1024, -(-maxp // ns))
-        ns = -(-maxp // pps)
-        sink = torch.empty(w.batch * (w.num_kv_heads // hpw) * ns * 8, dtype=torch.int32, device=mant.device)
-
-        def probe(i, hpw=hpw, pps=pps, ns=ns, sink=sink):
-            slot = i % resident
-            hma.paged_read_probe(mant[2 * slot], expo[2 * slot], mant[2 * slot + 1], expo[2 * slot + 1],
-                                 pt_d, ctx_d, max_ctx, sink, num_kv_heads=w.num_kv_heads,
-                                 pages_per_split=pps, n_splits=ns, heads_per_workgroup=hpw, stream=stream)
-        us = _time_launches(torch, stream, probe, min(64, max(resident, 16)))
-        out[name] = {"us": round(us, 3), "GBps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
-                     "heads_per_workgroup": hpw, "pages_per_split": pps, "splits": ns}
-    buf = torch.empty(1 << 30, dtype=torch.uint8, device=mant.device)
+    n16 = -(-kv_bytes // 16) * 16
+    buf = torch.empty(3 * n16, dtype=torch.uint8, device=dev)
     buf.fill_(3)
     nwg = 4096
-    sink = torch.empty(nwg * 4, dtype=torch.int32, device=mant.device)
+    sink = torch.empty(nwg * 4, dtype=torch.int32, device=dev)
+    us = _time_launches(torch, stream, lambda i: hma.stream_read_probe(
+        buf[(i % 3) * n16:(i % 3 + 1) * n16], sink, nwg, stream=stream), 30)
+    out["stream_same_bytes"] = {"us": round(us, 3), "GBps": round(kv_bytes / (us * 1e-6) / 1e9, 1)}
+    out["attn_over_stream_same_bytes"] = round(attn_us / us, 4)
+    del buf
+    if w.ctx[0] == "uniform":
+        for name, hpw, pps in (("attn_decomposition", 1, tps // w.page_size),
+                               ("heads_together", w.num_kv_heads, None)):
+            if pps is None:                     # about one workgroup per CU
+                ns = max(1, -(-256 // w.batch))
+                pps = min(1024, -(-maxp // ns))
+            ns = -(-maxp // pps)
+            sink = torch.empty(w.batch * (w.num_kv_heads // hpw) * ns * 8, dtype=torch.int32, device=dev)
+
+            def probe(i, hpw=hpw, pps=pps, ns=ns, sink=sink):
+                slot = i % resident
+                hma.paged_read_probe(mant[2 * slot], expo[2 * slot], mant[2 * slot + 1], expo[2 * slot + 1],
+                                     pt_d, ctx_d, max_ctx, sink, num_kv_heads=w.num_kv_heads,
+                                     pages_per_split=pps, n_splits=ns, heads_per_workgroup=hpw, stream=stream)
+            us = _time_launches(torch, stream, probe, min(64, max(resident, 16)))
+            out[name] = {"us": round(us, 3), "GBps": round(kv_bytes / (us * 1e-6) / 1e9, 1),
+                         "heads_per_workgroup": hpw, "pages_per_split": pps, "splits": ns}
+            out["attn_over_" + name] = round(attn_us / us, 4)
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    buf.fill_(3)
+    sink = torch.empty(nwg * 4, dtype=torch.int32, device=dev)
     us = _time_launches(torch, stream, lambda i: hma.stream_read_probe(buf, sink, nwg, stream=stream), 10)
     out["stream_1GiB"] = {"us": round(us, 1), "GBps": round((1 << 30) / (us * 1e-6) / 1e9, 1)}
     del buf
-    out["attn_frac_of_attn_decomposition"] = round(attn_gbps / out["attn_decomposition"]["GBps"], 4)
     return out
 
 
@@ -774,7 +789,7 @@ def main():
     legs = not mixed and not all_bf16 and not args.no_legs
     if legs:
         res["read_ceiling"] = read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident,
-                                           stream, attn_gbps)
+                                           stream, attn_mean)
         res["route_legs"] = route_legs(w, hma, torch, total_pages, pt_d, ctx_d, max_ctx, q, tps_arg, scale,
                                        stream, a_bytes)
     # a plain 1 GiB device copy on the same box: the attention rate as a
