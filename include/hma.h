@@ -413,7 +413,7 @@ HMA_API int hma_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, co
 /*
  * hma_stream_read_probe reads `bytes` contiguous bytes (a positive multiple
  * of 16, `buf` 16-byte aligned) with non-temporal 128-bit loads over
- * n_workgroups workgroups of 4 waves (grid-stride).
+ * n_workgroups workgroups of 4 waves, each reading its own contiguous range.
  *   sink        device uint32 [n_workgroups * 4]; sink_words is its length
  * Returns HMA_EINVAL for a NULL or misaligned buffer, bytes not a positive
  * multiple of 16, n_workgroups outside [1, 1048576] or a short sink.

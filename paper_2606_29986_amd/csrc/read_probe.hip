@@ -37,9 +37,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t probe_rsrc(const void *base, u
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes, 0x00020000);
 }
 
-// One lane's share of the four tiles of (page entry, KV head j): 32 bytes of
-// each mantissa tile and one exponent word (lanes 0-31 of K, 32-63 of V; the
-// other half's offset is past its resource and reads zero).  A dead slot gets
+// One lane's share of the four tiles of (page entry, KV head j): 16 bytes
+// of each half of each mantissa tile (each load instruction reads 1 KB of
+// whole 64-byte lines) and one exponent word (lanes 0-31 of K, 32-63 of V;
+// the other half's offset is past its resource and reads zero).  A dead slot gets
 // empty resources: the loads are issued but read nothing.
 __device__ __forceinline__ TileWords load_tiles(const PagedProbeParams &p, uint32_t ent, bool live, int j,
                                                 int lane)
@@ -51,12 +52,12 @@ __device__ __forceinline__ TileWords load_tiles(const PagedProbeParams &p, uint3
     const __amdgpu_buffer_rsrc_t vm = probe_rsrc(p.v_mant + tile * kTileMant, nm);
     const __amdgpu_buffer_rsrc_t kx = probe_rsrc(p.k_exp + tile * kTileExp, ne);
     const __amdgpu_buffer_rsrc_t vx = probe_rsrc(p.v_exp + tile * kTileExp, ne);
-    const uint32_t off = (uint32_t)lane * 32u;
+    const uint32_t off = (uint32_t)lane * 16u;
     TileWords t;
     t.k0 = __builtin_amdgcn_raw_buffer_load_b128(km, off, 0, kNonTemporal);
-    t.k1 = __builtin_amdgcn_raw_buffer_load_b128(km, off + 16u, 0, kNonTemporal);
+    t.k1 = __builtin_amdgcn_raw_buffer_load_b128(km, off + 1024u, 0, kNonTemporal);
     t.v0 = __builtin_amdgcn_raw_buffer_load_b128(vm, off, 0, kNonTemporal);
-    t.v1 = __builtin_amdgcn_raw_buffer_load_b128(vm, off + 16u, 0, kNonTemporal);
+    t.v1 = __builtin_amdgcn_raw_buffer_load_b128(vm, off + 1024u, 0, kNonTemporal);
     const uint32_t ek = __builtin_amdgcn_raw_buffer_load_b32(kx, lane < 32 ? (uint32_t)lane * 4u : (uint32_t)kTileExp,
                                                              0, kNonTemporal);
     const uint32_t ev = __builtin_amdgcn_raw_buffer_load_b32(vx, lane >= 32 ? (uint32_t)(lane - 32) * 4u
@@ -129,17 +130,21 @@ constexpr int kStreamThreads = 256;
 __global__ __launch_bounds__(kStreamThreads) void stream_read_probe_kernel(const u32x4_t *buf, uint64_t n16,
                                                                            uint32_t *sink)
 {
-    const uint64_t nthreads = (uint64_t)gridDim.x * kStreamThreads;
-    uint64_t i = (uint64_t)blockIdx.x * kStreamThreads + threadIdx.x;
+    // workgroup w reads its own contiguous range of 16-byte chunks, 4 KB per
+    // load instruction of the workgroup and four of them in flight
+    const uint64_t per = (n16 + gridDim.x - 1) / gridDim.x;
+    const uint64_t lo = (uint64_t)blockIdx.x * per;
+    const uint64_t hi = lo + per < n16 ? lo + per : n16;
     u32x4_t acc = {0u, 0u, 0u, 0u};
-    for (; i + 3 * nthreads < n16; i += 4 * nthreads) {
+    uint64_t i = lo + threadIdx.x;
+    for (; i + 3 * kStreamThreads < hi; i += 4 * kStreamThreads) {
         const u32x4_t a = __builtin_nontemporal_load(buf + i);
-        const u32x4_t b = __builtin_nontemporal_load(buf + i + nthreads);
-        const u32x4_t c = __builtin_nontemporal_load(buf + i + 2 * nthreads);
-        const u32x4_t d = __builtin_nontemporal_load(buf + i + 3 * nthreads);
+        const u32x4_t b = __builtin_nontemporal_load(buf + i + kStreamThreads);
+        const u32x4_t c = __builtin_nontemporal_load(buf + i + 2 * kStreamThreads);
+        const u32x4_t d = __builtin_nontemporal_load(buf + i + 3 * kStreamThreads);
         acc ^= a ^ b ^ c ^ d;
     }
-    for (; i < n16; i += nthreads)
+    for (; i < hi; i += kStreamThreads)
         acc ^= __builtin_nontemporal_load(buf + i);
     const uint32_t x = wave_xor(acc.x ^ acc.y ^ acc.z ^ acc.w);
     if ((threadIdx.x & 63) == 0)
