@@ -238,16 +238,17 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *   - with tokens_per_split = 0, when the batch needs more workgroups than
  *     one per compute unit (4-wave shape), the kernel cuts the pages of the
  *     whole batch, per KV head and in sequence order, into equal chunks, one
- *     per resident workgroup, built on the device from the lengths; a chunk
- *     that spans several sequences yields one range per sequence.  Ragged
- *     batches therefore load every compute unit equally.  Otherwise the
- *     ranges are tokens_per_split tokens of the library's choice.
+ *     per workgroup of a grid of min(2, resident workgroups per CU) x CUs,
+ *     built on the device from the lengths; a chunk that spans several
+ *     sequences yields one range per sequence.  Ragged batches therefore
+ *     load every compute unit equally.  Otherwise the ranges are
+ *     tokens_per_split tokens of the library's choice.
  * A ragged batch needs no host-side length information, and the schedule
  * depends only on the lengths: repeated calls give the same bits.  (The
- * number of chunks follows the resident workgroups of the kernel variant
- * that runs -- with or without BF16 pools -- so the same batch read with
- * and without BF16 pools may differ in the last bits; each is
- * deterministic.)
+ * number of chunks follows the occupancy of the kernel variant that runs --
+ * with or without BF16 pools -- so where the two variants' occupancies
+ * differ, the same batch read with and without BF16 pools may differ in the
+ * last bits; each is deterministic.)
  * context_lens[b] == 0 gives out = 0 and lse = -inf.  Slots at
  * or past the context end in the last page are never used, whatever they
  * hold.

@@ -1150,28 +1150,32 @@ __global__ __launch_bounds__(64 * WAVES, (WAVES == 4 && !MIXED) ? 3 : 2) void de
     attend_split<MIXED, WAVES>(p, b, j, split_piece(p, b, j, s, ctx), sm_buf, sm_pt);
 }
 
-// Workgroups of the 4-wave kernel the whole chip holds at once (occupancy per
-// compute unit times compute units), queried once per device and variant.
-int resident_workgroups(bool mixed)
+// Occupancy of the 4-wave kernel: workgroups per CU and CUs, queried once
+// per device and variant (0 workgroups on failure).
+struct Residency {
+    int per_cu, cus;
+};
+
+Residency resident_workgroups(bool mixed)
 {
     constexpr int kMaxDevices = 64;
-    static std::atomic<int> cache[kMaxDevices][2];
+    static std::atomic<int> cache[kMaxDevices][2][2];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
-        return 0;
-    int n = cache[dev][mixed].load(std::memory_order_relaxed);
-    if (n > 0)
-        return n;
-    int per_cu = 0, cus = 0;
+        return Residency{0, 0};
+    Residency r{cache[dev][mixed][0].load(std::memory_order_relaxed),
+                cache[dev][mixed][1].load(std::memory_order_relaxed)};
+    if (r.per_cu > 0 && r.cus > 0)
+        return r;
     const hipError_t e =
-        mixed ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_attn_bfp8_kernel<true, 4>, 256, 0)
-              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_attn_bfp8_kernel<false, 4>, 256, 0);
+        mixed ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&r.per_cu, decode_attn_bfp8_kernel<true, 4>, 256, 0)
+              : hipOccupancyMaxActiveBlocksPerMultiprocessor(&r.per_cu, decode_attn_bfp8_kernel<false, 4>, 256, 0);
     if (e != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return 0;
-    n = per_cu * cus;
-    cache[dev][mixed].store(n, std::memory_order_relaxed);
-    return n;
+        hipDeviceGetAttribute(&r.cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return Residency{0, 0};
+    cache[dev][mixed][0].store(r.per_cu, std::memory_order_relaxed);
+    cache[dev][mixed][1].store(r.cus, std::memory_order_relaxed);
+    return r;
 }
 
 int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
@@ -1208,12 +1212,17 @@ int launch_decode_attn(const AttnLaunch &a, hipStream_t stream)
     const bool mixed = a.k_bf16 != nullptr && a.v_bf16 != nullptr;
     dim3 grid((unsigned)blocks);
     if (a.planned) {
-        const int64_t resident = resident_workgroups(mixed);
+        const Residency r = resident_workgroups(mixed);
+        const int64_t resident = (int64_t)r.per_cu * r.cus;
         if (resident < 1)
             return -1;
-        // balanced: one chunk per resident workgroup; split schedule: two
-        // rounds of the resident workgroups over the split list
-        grid = a.balanced ? dim3((unsigned)std::min<int64_t>(resident, kBalancedGridCap))
+        // balanced: one chunk per workgroup, at most two workgroups per CU
+        // (a third per CU means shorter chunks, so more sequences cut into
+        // pieces that each pay a merge; measured slower), and a whole number
+        // of workgroups per CU; split schedule: two rounds of the resident
+        // workgroups over the split list
+        const int64_t balanced_grid = (int64_t)std::min(r.per_cu, 2) * r.cus;
+        grid = a.balanced ? dim3((unsigned)std::min<int64_t>(balanced_grid, kBalancedGridCap))
                           : dim3((unsigned)std::min(blocks, 2 * resident));
     }
     if (a.waves == 8) {
