@@ -439,6 +439,25 @@ def encoded_values_leg(w, hma, torch, kv, tps, stream, a_bytes):
             "encoded_packed_route_share": round(packed_route_share(kv), 4)}
 
 
+def valu_leg(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, q, scale, resident, stream, a_bytes, attn_us):
+    """The same attention launches (resident layers cycled, automatic ranges)
+    through libhma's vector-ALU comparison kernel, which runs both products on
+    v_dot2c / FMA instead of the matrix cores; valu_over_mfma = its time per
+    launch / the fused kernel's."""
+    dev = q.device
+    n = hma.valu_workspace_bytes(w.batch, w.num_q_heads, w.num_kv_heads, max_ctx)
+    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=dev)
+    o = torch.empty((w.batch, w.num_q_heads, w.head_dim), dtype=torch.int16, device=dev)
+
+    def launch(i):
+        s = i % resident
+        hma.decode_attn_bfp8_valu(q[s], mant[2 * s], expo[2 * s], mant[2 * s + 1], expo[2 * s + 1], pt_d, ctx_d,
+                                  max_ctx, o, ws, scale=scale, num_kv_heads=w.num_kv_heads, stream=stream)
+    us = _time_launches(torch, stream, launch, min(64, max(resident, 16)))
+    return {"valu_us": round(us, 3), "valu_GBps": round(a_bytes / (us * 1e-6) / 1e9, 1),
+            "valu_over_mfma": round(us / attn_us, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -792,6 +811,9 @@ def main():
                                            stream, attn_mean)
         res["route_legs"] = route_legs(w, hma, torch, total_pages, pt_d, ctx_d, max_ctx, q, tps_arg, scale,
                                        stream, a_bytes)
+        if w.num_q_heads // w.num_kv_heads <= 8:
+            res["valu_leg"] = valu_leg(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, q, scale, resident,
+                                       stream, a_bytes, attn_mean)
     # a plain 1 GiB device copy on the same box: the attention rate as a
     # fraction of what a copy (read + write) reaches here
     cp_a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)

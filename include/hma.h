@@ -426,6 +426,50 @@ HMA_API int hma_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, co
 HMA_API int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workgroups, uint32_t *sink,
                                   size_t sink_words, void *stream);
 
+/*
+ * hma_decode_attn_bfp8_valu -- measurement, not for production: the fused
+ * attention of hma_decode_attn_bfp8 over BFP8 pages (Sec. 3.3: the pages
+ * decoded exactly in registers inside the paged read) with both products on
+ * the vector ALU instead of the matrix cores, the comparison point for that
+ * choice.  Same reads, decode routes and split decomposition (one
+ * workgroup of 8 waves per (range, sequence, KV head)); QK^T runs on
+ * v_dot2c_f32_bf16 (BF16 pairs, float32 sums), PV on float32 FMAs with
+ * unrounded weights.  The ranges' partials are merged by log-sum-exp in a
+ * second kernel.  The result is the function of hma_decode_attn_bfp8 (same
+ * tolerance against exact arithmetic); the bits differ, since the sums run
+ * in another order.
+ *
+ * Arguments as hma_decode_attn_bfp8, with these restrictions: BFP8 pools
+ * only (page table entries are read as BFP8 page ids; the HMA_PAGE_BF16 tag
+ * is ignored), key_order 0, num_q_heads / num_kv_heads <= 8
+ * (HMA_EUNSUPPORTED otherwise).  tokens_per_split = 0 lets the library cut
+ * every sequence into ranges of one length, from max_context_len: the
+ * length that gives the batch one workgroup per compute unit, rounded up to
+ * a multiple of 16 and at most 4096 (a static grid: a ragged batch is not
+ * balanced across compute units); else a positive multiple of 16, at most
+ * 16384.
+ *   workspace  device buffer of at least hma_decode_attn_valu_workspace_bytes()
+ *              bytes for the same sizes, 256-byte aligned; every call writes
+ *              all of it before reading it (no zero fill needed).
+ * Errors: HMA_EINVAL, HMA_EUNSUPPORTED, HMA_EWORKSPACE, HMA_EHIP.
+ */
+HMA_API int hma_decode_attn_bfp8_valu(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp,
+                                      const uint8_t *v_mant, const uint8_t *v_exp, const int32_t *page_table,
+                                      int32_t max_pages_per_seq, const int32_t *context_lens,
+                                      int32_t max_context_len, int32_t batch, int32_t num_q_heads,
+                                      int32_t num_kv_heads, int32_t head_dim, int32_t page_size, float scale,
+                                      int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
+                                      size_t workspace_bytes, void *stream);
+
+/*
+ * Workspace bytes of hma_decode_attn_bfp8_valu (host only): (2 + 128)
+ * floats per (sequence, query head, range), the (max, sum) pairs first, the
+ * region padded to 256 bytes.  Returns (size_t)-1 on invalid or unsupported
+ * sizes, 0 for batch 0.
+ */
+HMA_API size_t hma_decode_attn_valu_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                                    int32_t max_context_len, int32_t tokens_per_split);
+
 /* Static, never-NULL description of a status code. */
 HMA_API const char *hma_status_string(int status);
 

@@ -74,6 +74,11 @@ def lib() -> ctypes.CDLL:
     L.hma_paged_read_probe.restype = ctypes.c_int
     L.hma_stream_read_probe.argtypes = [vp, sz, i32, vp, sz, vp]
     L.hma_stream_read_probe.restype = ctypes.c_int
+    L.hma_decode_attn_bfp8_valu.argtypes = [vp, vp, vp, vp, vp, vp, i32, vp, i32, i32, i32, i32, i32, i32,
+                                            ctypes.c_float, i32, vp, vp, vp, sz, vp]
+    L.hma_decode_attn_bfp8_valu.restype = ctypes.c_int
+    L.hma_decode_attn_valu_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
+    L.hma_decode_attn_valu_workspace_bytes.restype = sz
     L.hma_status_string.argtypes = [ctypes.c_int]
     L.hma_status_string.restype = ctypes.c_char_p
     _lib = L
@@ -296,6 +301,37 @@ def decode_attn_bfp8_noalloc(q, k_mant, k_exp, v_mant, v_exp, page_table, contex
         int(tokens_per_split), _ptr(out), _ptr(lse), _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_decode_attn_bfp8_noalloc")
+
+
+def valu_workspace_bytes(batch: int, num_q_heads: int, num_kv_heads: int, max_context_len: int,
+                         tokens_per_split: int = 0) -> int:
+    """hma_decode_attn_valu_workspace_bytes."""
+    n = int(lib().hma_decode_attn_valu_workspace_bytes(batch, num_q_heads, num_kv_heads,
+                                                       max_context_len, tokens_per_split))
+    if n == (1 << 64) - 1:
+        raise HmaError(HMA_EINVAL, "hma_decode_attn_valu_workspace_bytes")
+    return n
+
+
+def decode_attn_bfp8_valu(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len,
+                          out, workspace, lse=None, scale=None, num_kv_heads=None, tokens_per_split=0,
+                          head_dim=HEAD_DIM, page_size=PAGE_SIZE, stream=None) -> None:
+    """hma_decode_attn_bfp8_valu: decode_attn_bfp8 over BFP8 pages with both
+    products on the vector ALU (a measured comparison point, not for
+    production).  workspace: uint8 device tensor of valu_workspace_bytes()."""
+    _check_dev(q, k_mant, k_exp, v_mant, v_exp, page_table, context_lens, out, lse, workspace)
+    B, Hq, D = q.shape
+    hkv = int(num_kv_heads if num_kv_heads is not None else k_mant.shape[1])
+    if scale is None:
+        scale = 1.0 / (D ** 0.5)
+    ws_bytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    rc = lib().hma_decode_attn_bfp8_valu(
+        _ptr(q), _ptr(k_mant), _ptr(k_exp), _ptr(v_mant), _ptr(v_exp), _ptr(page_table),
+        int(page_table.shape[1]), _ptr(context_lens), int(max_context_len), B, Hq, hkv, D, page_size,
+        float(scale), int(tokens_per_split), _ptr(out), _ptr(lse), _ptr(workspace), ws_bytes,
+        _stream(stream))
+    if rc != HMA_OK:
+        raise HmaError(rc, "hma_decode_attn_bfp8_valu")
 
 
 def paged_read_probe(k_mant, k_exp, v_mant, v_exp, page_table, context_lens, max_context_len, sink,

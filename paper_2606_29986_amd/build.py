@@ -19,7 +19,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libhma.so")
 
-SOURCES = ["hma_api.cpp", "bfp8_dequant.hip", "decode_attn.hip", "rebuild_tiled.hip", "read_probe.hip"]
+SOURCES = ["hma_api.cpp", "bfp8_dequant.hip", "decode_attn.hip", "rebuild_tiled.hip", "read_probe.hip",
+           "valu_attn.hip"]
 ARCH = "gfx950"
 
 

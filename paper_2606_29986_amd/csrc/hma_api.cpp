@@ -153,6 +153,49 @@ size_t align256(size_t x)
     return (x + 255) & ~(size_t)255;
 }
 
+// ---- vector-ALU comparison kernel: at most 8 query heads per KV head, one
+// range length for the whole batch
+constexpr int32_t kValuMaxGroup = 8;
+
+bool valu_sizes_ok(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx, int32_t tps)
+{
+    return attn_sizes_ok(batch, hq, hkv, max_ctx) && hq / hkv <= kValuMaxGroup && tps >= 0 &&
+           tps % kSplitQuantum == 0 && tps <= hma::kMaxTokensPerSplit;
+}
+
+// Automatic range length: one workgroup per compute unit over the batch at
+// max_ctx (the kernel's registers leave room for one 8-wave workgroup per
+// CU), at most 4096 tokens per range so that a long sequence of a ragged
+// batch is spread over several CUs.
+constexpr int64_t kValuMaxAutoSplit = 4096;
+
+int32_t valu_tokens_per_split(int32_t batch, int32_t hkv, int32_t max_ctx, int32_t tps)
+{
+    if (tps)
+        return tps;
+    const int64_t pairs = (int64_t)batch * hkv;
+    const int64_t len = std::max(max_ctx, 1);
+    int64_t t = pairs >= kComputeUnits ? len : (pairs * len + kComputeUnits - 1) / kComputeUnits;
+    t = std::min(std::min(t, len), kValuMaxAutoSplit);
+    return round_up(t, kSplitQuantum);
+}
+
+struct ValuPlan {
+    int32_t tps, n_splits;
+    size_t ml_bytes, o_bytes;
+};
+
+ValuPlan valu_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx, int32_t tokens_per_split)
+{
+    ValuPlan pl;
+    pl.tps = valu_tokens_per_split(batch, hkv, max_ctx, tokens_per_split);
+    pl.n_splits = splits_for(max_ctx, pl.tps);
+    const size_t slots = (size_t)batch * hq * pl.n_splits;
+    pl.ml_bytes = align256(slots * 2 * sizeof(float));
+    pl.o_bytes = slots * kSupportedHeadDim * sizeof(float);
+    return pl;
+}
+
 AttnPlan attn_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx, int32_t tokens_per_split)
 {
     AttnPlan pl;
@@ -573,6 +616,50 @@ int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workgroups, u
     if (sink_words < (size_t)n_workgroups * 4)
         return HMA_EINVAL;
     return hma::launch_stream_read_probe(buf, bytes, sink, n_workgroups, static_cast<hipStream_t>(stream)) == 0
+               ? HMA_OK
+               : HMA_EHIP;
+}
+
+size_t hma_decode_attn_valu_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                            int32_t max_context_len, int32_t tokens_per_split)
+{
+    if (!valu_sizes_ok(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split))
+        return (size_t)-1;
+    if (batch == 0)
+        return 0;
+    const ValuPlan pl = valu_plan(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split);
+    return pl.ml_bytes + pl.o_bytes;
+}
+
+int hma_decode_attn_bfp8_valu(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
+                              const uint8_t *v_exp, const int32_t *page_table, int32_t max_pages_per_seq,
+                              const int32_t *context_lens, int32_t max_context_len, int32_t batch,
+                              int32_t num_q_heads, int32_t num_kv_heads, int32_t head_dim, int32_t page_size,
+                              float scale, int32_t tokens_per_split, uint16_t *out, float *lse, void *workspace,
+                              size_t workspace_bytes, void *stream)
+{
+    const int st = attn_check(q, k_mant, k_exp, v_mant, v_exp, nullptr, nullptr, page_table, max_pages_per_seq,
+                              context_lens, max_context_len, batch, num_q_heads, num_kv_heads, head_dim,
+                              page_size, scale, 0, tokens_per_split, out, lse);
+    if (st != HMA_OK)
+        return st;
+    if (num_q_heads / num_kv_heads > kValuMaxGroup)
+        return HMA_EUNSUPPORTED;
+    if (batch == 0)
+        return HMA_OK;
+    const ValuPlan pl = valu_plan(batch, num_q_heads, num_kv_heads, max_context_len, tokens_per_split);
+    if ((int64_t)batch * num_kv_heads * pl.n_splits > (int64_t)INT_MAX)
+        return HMA_EINVAL;
+    if (workspace == nullptr || workspace_bytes < pl.ml_bytes + pl.o_bytes)
+        return HMA_EWORKSPACE;
+    if (!aligned(workspace, 256))
+        return HMA_EINVAL;
+    uint8_t *ws = static_cast<uint8_t *>(workspace);
+    return hma::launch_decode_attn_valu(q, k_mant, k_exp, v_mant, v_exp, page_table, max_pages_per_seq,
+                                        context_lens, max_context_len, batch, num_q_heads, num_kv_heads, scale,
+                                        pl.tps, pl.n_splits, reinterpret_cast<float *>(ws),
+                                        reinterpret_cast<float *>(ws + pl.ml_bytes), out, lse,
+                                        static_cast<hipStream_t>(stream)) == 0
                ? HMA_OK
                : HMA_EHIP;
 }

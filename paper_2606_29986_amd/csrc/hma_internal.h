@@ -95,4 +95,14 @@ int launch_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, const u
 int launch_stream_read_probe(const void *buf, uint64_t bytes, uint32_t *sink, int32_t n_workgroups,
                              hipStream_t stream);
 
+// Vector-ALU decode attention (valu_attn.hip): per split a partial kernel
+// (grid batch * hkv * n_splits), then a merge kernel (grid batch * hkv).
+// part_ml holds batch * hkv * n_splits * g * 2 floats, part_o
+// batch * hkv * n_splits * g * 128; every slot is written each call.
+int launch_decode_attn_valu(const uint16_t *q, const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
+                            const uint8_t *v_exp, const int32_t *page_table, int32_t max_pages,
+                            const int32_t *ctx, int32_t max_ctx, int32_t batch, int32_t hq, int32_t hkv,
+                            float scale, int32_t tps, int32_t n_splits, float *part_ml, float *part_o,
+                            uint16_t *out, float *lse, hipStream_t stream);
+
 }  // namespace hma

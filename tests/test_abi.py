@@ -30,7 +30,8 @@ def test_header_declares_the_boundary():
                             "hma_decode_attn_bfp8", "hma_decode_attn_bfp8_noalloc",
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
                             "hma_ingress_rebuild", "hma_status_string", "hma_validate_page_table",
-                            "hma_paged_read_probe", "hma_stream_read_probe"])
+                            "hma_paged_read_probe", "hma_stream_read_probe",
+                            "hma_decode_attn_bfp8_valu", "hma_decode_attn_valu_workspace_bytes"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -334,3 +335,53 @@ def test_read_probe_validation():
     assert stream(nwg=0) == hma.HMA_EINVAL
     assert stream(nwg=(1 << 20) + 1) == hma.HMA_EINVAL
     assert stream(sink_words=255) == hma.HMA_EINVAL
+
+
+def test_valu_attn_validation_and_workspace():
+    """The vector-ALU comparison kernel: BFP8 pools only, groups up to 8, a
+    workspace of (2 + 128) floats per (sequence, query head, range) with the
+    (max, sum) region padded to 256 bytes; every check before any HIP call."""
+    L = hma.lib()
+    # automatic ranges: one workgroup per compute unit (256) over the batch at
+    # max_context_len, whole pages, at most 4096 tokens
+    def auto_splits(B, Hkv, ctx):
+        tps = min(-(-B * Hkv * ctx // 256), ctx, 4096)
+        return -(-ctx // (-(-tps // 16) * 16))
+    B, Hq, Hkv, ctx = 16, 64, 8, 8192
+    S = auto_splits(B, Hkv, ctx)
+    assert S == 2
+    assert hma.valu_workspace_bytes(B, Hq, Hkv, ctx) == (B * Hq * S * 8 + 255) // 256 * 256 + B * Hq * S * 512
+    # as many pairs as compute units: one range per sequence up to 4096 tokens
+    assert hma.valu_workspace_bytes(64, 64, 8, 2400) == 64 * 64 * 8 + 64 * 64 * 512
+    assert hma.valu_workspace_bytes(64, 64, 8, 9000) == 3 * (64 * 64 * 8 + 64 * 64 * 512)
+    # a small batch: ranges of ceil(B * Hkv * ctx / 256) tokens rounded up to whole pages
+    assert auto_splits(1, 8, 8000) == 32
+    assert hma.valu_workspace_bytes(1, 64, 8, 8000) == (64 * 32 * 8 + 255) // 256 * 256 + 64 * 32 * 512
+    # explicit ranges
+    assert hma.valu_workspace_bytes(B, Hq, Hkv, ctx, 1024) == B * Hq * 8 * 8 + B * Hq * 8 * 512
+    assert hma.valu_workspace_bytes(0, Hq, Hkv, ctx) == 0
+    for bad in ((B, 60, Hkv, ctx, 0), (B, 16 * 9, 16, ctx, 0), (B, Hq, Hkv, ctx, 40), (B, Hq, Hkv, -1, 0),
+                (B, Hq, Hkv, ctx, 16400)):
+        with pytest.raises(hma.HmaError):
+            hma.valu_workspace_bytes(*bad)
+
+    need = hma.valu_workspace_bytes(B, Hq, Hkv, ctx)
+
+    def call(q=FAKE, maxp=512, maxctx=ctx, Hq=Hq, Hkv=Hkv, D=128, P=16, tps=0, ws=FAKE, wsb=need, lse=None,
+             scale=0.088388346, Bn=B):
+        return L.hma_decode_attn_bfp8_valu(q, FAKE, FAKE, FAKE, FAKE, FAKE, maxp, FAKE, maxctx, Bn, Hq, Hkv, D, P,
+                                           scale, tps, FAKE, lse, ws, wsb, None)
+    assert call(ws=None) == hma.HMA_EWORKSPACE
+    assert call(wsb=need - 1) == hma.HMA_EWORKSPACE
+    assert call(ws=MISALIGNED) == hma.HMA_EINVAL
+    assert call(Hq=16 * 9, Hkv=16) == hma.HMA_EUNSUPPORTED      # group of 9
+    assert call(Hq=60) == hma.HMA_EINVAL
+    assert call(D=64) == hma.HMA_EUNSUPPORTED
+    assert call(P=32) == hma.HMA_EUNSUPPORTED
+    assert call(tps=40) == hma.HMA_EINVAL
+    assert call(maxp=100) == hma.HMA_EINVAL
+    assert call(scale=float("nan")) == hma.HMA_EINVAL
+    assert call(q=None) == hma.HMA_EINVAL
+    assert call(q=MISALIGNED) == hma.HMA_EINVAL
+    assert call(lse=0x10002) == hma.HMA_EINVAL
+    assert call(Bn=0) == hma.HMA_OK
