@@ -237,12 +237,14 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *     shorter last splits);
  *   - with tokens_per_split = 0, when the batch needs more workgroups than
  *     one per compute unit (4-wave shape), the kernel cuts the pages of the
- *     whole batch, per KV head and in sequence order, into equal chunks, one
- *     per workgroup of a grid of min(2, resident workgroups per CU) x CUs,
- *     built on the device from the lengths; a chunk that spans several
- *     sequences yields one range per sequence.  Ragged batches therefore
- *     load every compute unit equally.  Otherwise the ranges are
- *     tokens_per_split tokens of the library's choice.
+ *     whole batch, per KV head and in sequence order, into equal chunks
+ *     built on the device from the lengths, for a grid of min(2, resident
+ *     workgroups per CU) x CUs: one chunk per wave when that gives chunks of
+ *     at least 128 pages (each wave then attends its pieces alone), else one
+ *     per workgroup; a chunk that spans several sequences yields one range
+ *     per sequence.  Ragged batches therefore load every compute unit
+ *     equally.  Otherwise the ranges are tokens_per_split tokens of the
+ *     library's choice.
  * A ragged batch needs no host-side length information, and the schedule
  * depends only on the lengths: repeated calls give the same bits.  (The
  * number of chunks follows the occupancy of the kernel variant that runs --

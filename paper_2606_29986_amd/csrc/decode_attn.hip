@@ -606,6 +606,83 @@ __device__ __forceinline__ void zero_pair_output(const AttnParams &p, int b, int
         p.lse[out_row] = -INFINITY;
 }
 
+// Q^T operand of lane (G, r): column r = query head j*g + r of row out_row
+// (zero for padded heads).  Keys kept in the interleaved rotary order (stored
+// channel 2i = key channel i, 2i + 1 = 64 + i) are met by permuting q the
+// same way once, here: stored channels c0..c0+7 take q[c0/2 ..] and
+// q[64 + c0/2 ..] in turn.
+__device__ __forceinline__ void q_operand(const AttnParams &p, int64_t out_row, int G, bool head_ok,
+                                          u32x4_t (&qB)[4])
+{
+    const uint16_t *qrow = p.q + out_row * kHeadDim;
+#pragma unroll
+    for (int kk = 0; kk < 4; kk++) {
+        const int c0 = qk_channel(G, kk);
+        u32x4_t v;
+        if (p.key_interleaved) {
+            const u32x2_t a = *reinterpret_cast<const u32x2_t *>(qrow + c0 / 2);
+            const u32x2_t b = *reinterpret_cast<const u32x2_t *>(qrow + kHeadDim / 2 + c0 / 2);
+            v = u32x4_t{__builtin_amdgcn_perm(b.x, a.x, kPermLoHalves), __builtin_amdgcn_perm(b.x, a.x, kPermHiHalves),
+                        __builtin_amdgcn_perm(b.y, a.y, kPermLoHalves), __builtin_amdgcn_perm(b.y, a.y, kPermHiHalves)};
+        } else {
+            v = *reinterpret_cast<const u32x4_t *>(qrow + c0);
+        }
+        qB[kk] = head_ok ? v : u32x4_t{0u, 0u, 0u, 0u};
+    }
+}
+
+// Online log-sum-exp fold of the n_parts published partials of one (b, j),
+// in piece order (the result must not depend on which workgroup or wave
+// arrived last), for accumulator columns col0 + q * step, q < NC; the next
+// piece's device-coherent loads are in flight while one is folded.  Partial
+// of piece t: columns [8][G 4][head g] of f32x4 at rs_o, (max, sum) per head
+// at rs_ml.
+template <int NC>
+__device__ __forceinline__ void fold_partials(__amdgpu_buffer_rsrc_t rs_o, __amdgpu_buffer_rsrc_t rs_ml, int n_parts,
+                                              int g, int G, int r, int col0, int step, f32x4_t (&F)[NC], float &Mf,
+                                              float &Lf)
+{
+    auto col_offset = [&](int t, int n) { return (uint32_t)((((t * 8 + n) * 4 + G) * g + r) * 16); };
+    Mf = -INFINITY;
+    Lf = 0.0f;
+#pragma unroll
+    for (int q = 0; q < NC; q++)
+        F[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    auto load_split = [&](int t, f32x4_t(&dst)[NC], u32x2_t &ml) {
+#pragma unroll
+        for (int q = 0; q < NC; q++)
+            dst[q] = __builtin_bit_cast(
+                f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, col_offset(t, col0 + q * step), 0, kCoherent));
+        ml = __builtin_amdgcn_raw_buffer_load_b64(rs_ml, (uint32_t)((t * g + r) * 8), 0, kCoherent);
+    };
+    auto fold = [&](const f32x4_t(&v)[NC], u32x2_t ml) {
+        const float mt = __uint_as_float(ml.x);
+        const float Mn = fmaxf(Mf, mt);
+        const float a = __builtin_amdgcn_exp2f(Mf - Mn);     // 0 for the first split
+        const float c = __builtin_amdgcn_exp2f(mt - Mn);
+        Lf = fmaf(Lf, a, __uint_as_float(ml.y) * c);
+        Mf = Mn;
+#pragma unroll
+        for (int q = 0; q < NC; q++)
+#pragma unroll
+            for (int i = 0; i < 4; i++)
+                F[q][i] = fmaf(F[q][i], a, v[q][i] * c);
+    };
+    // two register sets, alternating; past the end the last piece is
+    // re-read and not used
+    f32x4_t va[NC], vb[NC];
+    u32x2_t ma, mb;
+    load_split(0, va, ma);
+    for (int t = 0; t < n_parts; t += 2) {
+        load_split(min(t + 1, n_parts - 1), vb, mb);
+        fold(va, ma);
+        if (t + 1 >= n_parts)
+            break;
+        load_split(min(t + 2, n_parts - 1), va, ma);
+        fold(vb, mb);
+    }
+}
+
 // One piece of (sequence b, KV head j) (non-empty).  Every wave of the
 // workgroup calls it, and every wave meets the same barriers.
 template <bool MIXED, int WAVES>
@@ -634,28 +711,8 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
             sm_pt[i] = (uint32_t)pt[i];
     }
 
-    // Q^T operand (column r = head j*g + r; zero for padded heads).  Keys kept
-    // in the interleaved rotary order (stored channel 2i = key channel i,
-    // 2i + 1 = 64 + i) are met by permuting q the same way once, here:
-    // stored channels c0..c0+7 take q[c0/2 ..] and q[64 + c0/2 ..] in turn.
     u32x4_t qB[4];
-    {
-        const uint16_t *qrow = p.q + out_row * kHeadDim;
-#pragma unroll
-        for (int kk = 0; kk < 4; kk++) {
-            const int c0 = qk_channel(G, kk);
-            u32x4_t v;
-            if (p.key_interleaved) {
-                const u32x2_t a = *reinterpret_cast<const u32x2_t *>(qrow + c0 / 2);
-                const u32x2_t b = *reinterpret_cast<const u32x2_t *>(qrow + kHeadDim / 2 + c0 / 2);
-                v = u32x4_t{__builtin_amdgcn_perm(b.x, a.x, kPermLoHalves), __builtin_amdgcn_perm(b.x, a.x, kPermHiHalves),
-                            __builtin_amdgcn_perm(b.y, a.y, kPermLoHalves), __builtin_amdgcn_perm(b.y, a.y, kPermHiHalves)};
-            } else {
-                v = *reinterpret_cast<const u32x4_t *>(qrow + c0);
-            }
-            qB[kk] = head_ok ? v : u32x4_t{0u, 0u, 0u, 0u};
-        }
-    }
+    q_operand(p, out_row, G, head_ok, qB);
     __syncthreads();
 
     SoftmaxState st = {-INFINITY, 0.0f};
@@ -784,48 +841,9 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
         return;
 
     if (head_ok) {
-        // online log-sum-exp fold of every piece's partial, in piece order
-        // (the result must not depend on which workgroup arrived last); the
-        // next piece's device-coherent loads are in flight while one is folded
-        float Mf = -INFINITY, Lf = 0.0f;
+        float Mf, Lf;
         f32x4_t F[kCols];
-#pragma unroll
-        for (int q = 0; q < kCols; q++)
-            F[q] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        auto load_split = [&](int t, f32x4_t(&dst)[kCols], u32x2_t &ml) {
-#pragma unroll
-            for (int q = 0; q < kCols; q++)
-                dst[q] = __builtin_bit_cast(
-                    f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(rs_o, col_offset(t, wave + q * WAVES), 0,
-                                                                   kCoherent));
-            ml = __builtin_amdgcn_raw_buffer_load_b64(rs_ml, (uint32_t)((t * p.g + r) * 8), 0, kCoherent);
-        };
-        auto fold = [&](const f32x4_t(&v)[kCols], u32x2_t ml) {
-            const float mt = __uint_as_float(ml.x);
-            const float Mn = fmaxf(Mf, mt);
-            const float a = __builtin_amdgcn_exp2f(Mf - Mn);     // 0 for the first split
-            const float c = __builtin_amdgcn_exp2f(mt - Mn);
-            Lf = fmaf(Lf, a, __uint_as_float(ml.y) * c);
-            Mf = Mn;
-#pragma unroll
-            for (int q = 0; q < kCols; q++)
-#pragma unroll
-                for (int i = 0; i < 4; i++)
-                    F[q][i] = fmaf(F[q][i], a, v[q][i] * c);
-        };
-        // two register sets, alternating; past the end the last piece is
-        // re-read and not used
-        f32x4_t va[kCols], vb[kCols];
-        u32x2_t ma, mb;
-        load_split(0, va, ma);
-        for (int t = 0; t < n_parts; t += 2) {
-            load_split(min(t + 1, n_parts - 1), vb, mb);
-            fold(va, ma);
-            if (t + 1 >= n_parts)
-                break;
-            load_split(min(t + 2, n_parts - 1), va, ma);
-            fold(vb, mb);
-        }
+        fold_partials<kCols>(rs_o, rs_ml, n_parts, p.g, G, r, wave, WAVES, F, Mf, Lf);
         const float inv = 1.0f / Lf;
 #pragma unroll
         for (int q = 0; q < kCols; q++)
@@ -834,6 +852,106 @@ __device__ __forceinline__ void attend_split(const AttnParams &p, int b, int j, 
             p.lse[out_row] = (Mf + log2f(Lf)) * kLn2;
     }
     if (wave == 0 && lane == 0)     // ready for the next call
+        __hip_atomic_store(&p.tickets[pair_id], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One piece of (sequence b, KV head j) (non-empty) attended by one wave
+// alone (the page-balanced schedule): wpt holds the page-table entries of its
+// pages.  No barrier: a piece that is the whole context writes the output;
+// otherwise the wave publishes its partial (device-coherent) and the last
+// wave to arrive among the pieces of (b, j) folds all of them.
+template <bool MIXED>
+__device__ __forceinline__ void attend_wave_piece(const AttnParams &p, int b, int j, const Piece &pc,
+                                                  const uint32_t *wpt)
+{
+    const int lane = thread_index() & 63;
+    const int G = lane >> 4;
+    const int r = lane & 15;
+    const bool head_ok = r < p.g;
+    const int head = j * p.g + (head_ok ? r : 0);
+    const int64_t out_row = (int64_t)b * p.hq + head;
+    u32x4_t qB[4];
+    q_operand(p, out_row, G, head_ok, qB);
+
+    SoftmaxState st = {-INFINITY, 0.0f};
+    f32x4_t O[8];
+#pragma unroll
+    for (int n = 0; n < 8; n++)
+        O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // the register pipeline of attend_split, over every page of the piece
+    const int n_pages = (pc.n_tok + kPageSize - 1) / kPageSize;
+    auto page_at = [&](int k) {
+        const int kk = min(k, n_pages - 1);
+        PageInfo c;
+        c.nval = min(kPageSize, pc.n_tok - kk * kPageSize);
+        c.ent = __builtin_amdgcn_readfirstlane(wpt[kk]);
+        c.live = k < n_pages;
+        return c;
+    };
+    {
+        const LaneOffsets lo = lane_offsets(G, r);
+        PageRaw<MIXED> c0, c1;
+        PageInfo i0 = page_at(0), i1;
+        load_page_regs(c0, i0, p, j, lo);
+        for (int k = 0; k < n_pages; k += 2) {
+            i1 = page_at(k + 1);
+            load_page_regs(c1, i1, p, j, lo);
+            process_page<MIXED>(c0, i0, qB, p.scale_log2, G, st, O);
+            if (k + 1 >= n_pages)
+                break;
+            i0 = page_at(k + 2);
+            load_page_regs(c0, i0, p, j, lo);
+            process_page<MIXED>(c1, i1, qB, p.scale_log2, G, st, O);
+        }
+    }
+    const float L = sum_over_groups(st.l);
+    const float M = st.m;
+    uint16_t *orow = p.out + out_row * kHeadDim + 32 * G;
+    if (pc.n_parts == 1) {
+        if (head_ok) {
+            const float inv = 1.0f / L;
+#pragma unroll
+            for (int n = 0; n < 8; n++)
+                store_out_col(orow, n, O[n], inv);
+            if (p.lse && G == 0)
+                p.lse[out_row] = (M + log2f(L)) * kLn2;
+        }
+        return;
+    }
+    const int s = pc.idx;
+    const int64_t pair_id = (int64_t)b * p.hkv + j;
+    const __amdgpu_buffer_rsrc_t rs_o = raw_rsrc(p.part_o + pc.base * p.g * kHeadDim);
+    const __amdgpu_buffer_rsrc_t rs_ml = raw_rsrc(p.part_ml + pc.base * p.g);
+    if (head_ok) {
+#pragma unroll
+        for (int n = 0; n < 8; n++)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, O[n]), rs_o,
+                                                   (uint32_t)((((s * 8 + n) * 4 + G) * p.g + r) * 16), 0, kCoherent);
+        if (G == 0) {
+            const u32x2_t ml = {__float_as_uint(M), __float_as_uint(L)};
+            __builtin_amdgcn_raw_buffer_store_b64(ml, rs_ml, (uint32_t)((s * p.g + r) * 8), 0, kCoherent);
+        }
+    }
+    // every store of the wave has completed (device-coherent) before the ticket
+    __builtin_amdgcn_s_waitcnt(0);
+    int last = 0;
+    if (lane == 0)
+        last = __hip_atomic_fetch_add(&p.tickets[pair_id], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               pc.n_parts - 1;
+    if (!__builtin_amdgcn_readfirstlane(last))
+        return;
+    if (head_ok) {
+        float Mf, Lf;
+        f32x4_t F[8];
+        fold_partials<8>(rs_o, rs_ml, pc.n_parts, p.g, G, r, 0, 1, F, Mf, Lf);
+        const float inv = 1.0f / Lf;
+#pragma unroll
+        for (int n = 0; n < 8; n++)
+            store_out_col(orow, n, F[n], inv);
+        if (p.lse && G == 0)
+            p.lse[out_row] = (Mf + log2f(Lf)) * kLn2;
+    }
+    if (lane == 0)     // ready for the next call
         __hip_atomic_store(&p.tickets[pair_id], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -996,17 +1114,27 @@ __device__ __forceinline__ Plan build_plan(const AttnParams &p, int32_t *sm_ctx,
 
 // Page-balanced schedule (4-wave shape, automatic split length): the pages
 // of each KV head's sequences, taken in sequence order, form one list of T
-// pages that is cut into n_chunks chunks of C pages; item it = (chunk c, KV
-// head j) with the KV head fastest, and workgroup w takes items w, w + grid,
-// ...  With n_chunks = grid / Hkv every workgroup takes one item, so every
+// pages, cut into equal ranges on the device from the lengths, so every
 // compute unit gets the same number of pages whatever the length mix.  A
-// chunk that covers parts of several sequences yields one piece per
-// sequence; the pieces of (b, j) come from chunks c_first(b) .. c_last(b),
-// and piece c of sequence b is partial slot c + b of KV head j (unique: for
-// two pieces (c, b) and (c', b') with c + b = c' + b' the chunks and
-// sequences would have to overlap in opposite orders).  The chunking depends
-// only on the lengths, so the result does not depend on timing.
+// range that covers parts of several sequences yields one piece per
+// sequence; the pieces of (b, j) come from ranges k_first(b) .. k_last(b), and
+// piece k of sequence b is partial slot k + b of KV head j (unique: for two
+// pieces (k, b) and (k', b') with k + b = k' + b' the ranges and sequences
+// would have to overlap in opposite orders).  Two granularities:
+//   - one range per wave (items (range, KV head), KV head fastest; wave w of
+//     workgroup x takes items x * WAVES + w, + grid * WAVES, ...): no wave
+//     waits for another, and every piece is published by the wave alone.
+//     Taken when a wave's range is at least kWaveRangePages long, so that
+//     the pieces (one publish each, and a fold over them) are few against
+//     the pages;
+//   - otherwise one range (chunk) per workgroup, whose waves share each
+//     piece's pages and merge them in LDS (shorter ranges would cut most
+//     sequences into many published pieces).
+// The ranges depend only on the lengths, so the result does not depend on
+// timing.
 constexpr int kMinChunkPages = 16;
+constexpr int kMinWavePages = 4;
+constexpr int kWaveRangePages = 128;
 
 __device__ __forceinline__ void balanced_schedule_table(const AttnParams &p, int32_t *sm_pre)
 {
@@ -1028,23 +1156,80 @@ __device__ __forceinline__ void balanced_schedule_table(const AttnParams &p, int
     __syncthreads();
 }
 
-template <bool MIXED, int WAVES>
-__device__ __forceinline__ void balanced_schedule(const AttnParams &p, int32_t *sm_pre, uint8_t *sm_buf,
-                                                  uint32_t *sm_pt)
+// Piece (range k of W pages, sequence b) of KV head j, for a range [g0, g1)
+// of the list that overlaps sequence b's pages [pb0, pb1) (non-empty).
+__device__ __forceinline__ Piece range_piece(const AttnParams &p, int b, int j, int k, int W, int g0, int g1,
+                                             int pb0, int pb1)
 {
-    balanced_schedule_table(p, sm_pre);
+    const int lo = max(g0, pb0) - pb0;     // local pages [lo, hi)
+    const int hi = min(g1, pb1) - pb0;
+    const int k_first = pb0 / W;
+    const int k_last = (pb1 - 1) / W;
+    Piece pc;
+    pc.t_begin = lo * kPageSize;
+    pc.n_tok = min(context_len(p, b), hi * kPageSize) - pc.t_begin;
+    pc.idx = k - k_first;
+    pc.n_parts = k_last - k_first + 1;
+    pc.base = (int64_t)j * p.slots_per_head + k_first + b;
+    return pc;
+}
+
+// One range per wave.  wpt: LDS for WAVES x kMaxChunkPages page-table
+// entries (one slice per wave).
+template <bool MIXED, int WAVES>
+__device__ __forceinline__ void balanced_waves(const AttnParams &p, const int32_t *sm_pre, int T, int W,
+                                               uint32_t *sm_wpt)
+{
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int T = __builtin_amdgcn_readfirstlane(sm_pre[p.batch]);
-    // chunk length C: one item per workgroup, at least kMinChunkPages, at
-    // most the page-table slice an LDS staging holds
-    const int n0 = max(1, (int)gridDim.x / p.hkv);
-    const int C = min(kMaxSplitPages, max(kMinChunkPages, (T + n0 - 1) / n0));
+    const int n_ranges = min((T + W - 1) / W, p.slots_per_head - p.batch);     // host bound holds it
+    uint32_t *wpt = sm_wpt + wave * kMaxChunkPages;
+    const int n_items = n_ranges * p.hkv;
+    for (int it = (int)blockIdx.x * WAVES + wave; it < n_items; it += (int)gridDim.x * WAVES) {
+        const int k = it / p.hkv;
+        const int j = it - k * p.hkv;
+        const int g0 = k * W;
+        const int g1 = min(g0 + W, T);
+        const int b_first = row_of(sm_pre, p.batch, g0);
+        // this range's page-table entries: list page g0 + i at wpt[i]
+        const int lane = thread_index() & 63;     // not hoisted out of the item loop
+        for (int b = b_first; b < p.batch; b++) {
+            const int pb0 = __builtin_amdgcn_readfirstlane(sm_pre[b]);
+            if (pb0 >= g1)
+                break;
+            const int pb1 = __builtin_amdgcn_readfirstlane(sm_pre[b + 1]);
+            const int lo = max(g0, pb0);
+            const int hi = min(g1, pb1);
+            const int32_t *pt = p.page_table + (int64_t)b * p.max_pages + (lo - pb0);
+            for (int i = lane; i < hi - lo; i += 64)
+                wpt[lo - g0 + i] = (uint32_t)pt[i];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        for (int b = b_first; b < p.batch; b++) {
+            const int pb0 = __builtin_amdgcn_readfirstlane(sm_pre[b]);
+            const int pb1 = __builtin_amdgcn_readfirstlane(sm_pre[b + 1]);
+            if (pb0 >= g1)
+                break;
+            if (pb1 <= g0 || pb1 == pb0)
+                continue;     // an empty sequence has no piece (its zero output is written by the caller)
+            const Piece pc = range_piece(p, b, j, k, W, g0, g1, pb0, pb1);
+            attend_wave_piece<MIXED>(p, b, j, pc, wpt + (max(g0, pb0) - g0));
+        }
+        // the next item rewrites this wave's slice
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+}
+
+// One range (chunk of C pages) per workgroup: items (chunk, KV head), KV head
+// fastest; workgroup x takes items x, x + grid, ...
+template <bool MIXED, int WAVES>
+__device__ __forceinline__ void balanced_chunks(const AttnParams &p, const int32_t *sm_pre, int T, int C,
+                                                uint8_t *sm_buf, uint32_t *sm_pt)
+{
     const int n_chunks = min((T + C - 1) / C, p.slots_per_head - p.batch);     // host bound holds it
-    // empty sequences own a zero output
-    for (int b = blockIdx.x; b < p.batch; b += gridDim.x)
-        if (__builtin_amdgcn_readfirstlane(sm_pre[b + 1] - sm_pre[b]) == 0)
-            for (int j = wave; j < p.hkv; j += WAVES)
-                zero_pair_output(p, b, j);
     const int n_items = n_chunks * p.hkv;
     for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
         const int c = it / p.hkv;
@@ -1057,19 +1242,35 @@ __device__ __forceinline__ void balanced_schedule(const AttnParams &p, int32_t *
             if (pb0 >= g1)
                 break;
             if (pb1 <= g0 || pb1 == pb0)
-                continue;     // an empty sequence has no piece (its zero output is written above)
-            const int lo = max(g0, pb0) - pb0;     // local pages [lo, hi)
-            const int hi = min(g1, pb1) - pb0;
-            const int c_first = pb0 / C;
-            const int c_last = (pb1 - 1) / C;
-            Piece pc;
-            pc.t_begin = lo * kPageSize;
-            pc.n_tok = min(context_len(p, b), hi * kPageSize) - pc.t_begin;
-            pc.idx = c - c_first;
-            pc.n_parts = c_last - c_first + 1;
-            pc.base = (int64_t)j * p.slots_per_head + c_first + b;
+                continue;     // an empty sequence has no piece (its zero output is written by the caller)
+            const Piece pc = range_piece(p, b, j, c, C, g0, g1, pb0, pb1);
             attend_split<MIXED, WAVES>(p, b, j, pc, sm_buf, sm_pt);
         }
+    }
+}
+
+template <bool MIXED, int WAVES>
+__device__ __forceinline__ void balanced_schedule(const AttnParams &p, int32_t *sm_pre, uint8_t *sm_buf,
+                                                  uint32_t *sm_pt)
+{
+    balanced_schedule_table(p, sm_pre);
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int T = __builtin_amdgcn_readfirstlane(sm_pre[p.batch]);
+    // empty sequences own a zero output
+    for (int b = blockIdx.x; b < p.batch; b += gridDim.x)
+        if (__builtin_amdgcn_readfirstlane(sm_pre[b + 1] - sm_pre[b]) == 0)
+            for (int j = wave; j < p.hkv; j += WAVES)
+                zero_pair_output(p, b, j);
+    // range lengths: one item per wave (or per workgroup), at least a few
+    // pages, at most the page-table slice staged in LDS
+    const int n_wg = max(1, (int)gridDim.x / p.hkv);
+    const int W = min(kMaxChunkPages, max(kMinWavePages, (T + n_wg * WAVES - 1) / (n_wg * WAVES)));
+    if (W >= kWaveRangePages) {
+        static_assert(WAVES * kMaxChunkPages * 4 <= merge_bytes<WAVES>(), "page-table slices fit the merge LDS");
+        balanced_waves<MIXED, WAVES>(p, sm_pre, T, W, reinterpret_cast<uint32_t *>(sm_buf));
+    } else {
+        const int C = min(kMaxChunkPages, max(kMinChunkPages, (T + n_wg - 1) / n_wg));
+        balanced_chunks<MIXED, WAVES>(p, sm_pre, T, C, sm_buf, sm_pt);
     }
 }
 

@@ -205,15 +205,16 @@ AttnPlan attn_plan(int32_t batch, int32_t hq, int32_t hkv, int32_t max_ctx, int3
     pl.waves = waves_for(pairs * pl.n_splits);
     pl.planned = pl.waves == 4 && batch <= hma::kPlanMaxBatch && pl.n_splits < hma::kPlanMaxBatch;
     // with the automatic split, the 4-wave schedule cuts the batch's pages
-    // into equal chunks on the device (ragged batches balance across CUs)
+    // into equal ranges on the device, one per wave (ragged batches balance
+    // across CUs)
     pl.balanced = pl.planned && tokens_per_split == 0;
     pl.slots_per_head = 0;
     if (pl.balanced) {
-        // chunks per KV head: at most the grid's share (one chunk per
-        // workgroup), or the count of chunks of the largest size when the
-        // pages outnumber that; piece (c, b) is slot c + b
+        // ranges per KV head: at most the grid's share (one range per
+        // wave), or the count of ranges of the largest size when the pages
+        // outnumber that; piece (k, b) is slot k + b
         const int64_t max_pages = ((int64_t)max_ctx + kSupportedPageSize - 1) / kSupportedPageSize;
-        const int64_t by_grid = (hma::kBalancedGridCap + hkv - 1) / hkv;
+        const int64_t by_grid = (hma::kBalancedGridCap + hkv - 1) / hkv * hma::kBalancedWaves;
         const int64_t by_size = (batch * max_pages + hma::kMaxChunkPages - 1) / hma::kMaxChunkPages;
         pl.slots_per_head = (int32_t)(std::max(by_grid, by_size) + batch);
         pl.slots = (int64_t)hkv * pl.slots_per_head;

@@ -47,10 +47,13 @@ int launch_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_exp, ui
                            int32_t n_pools, int64_t dst_stride_pages, int32_t hkv, size_t mant_bytes,
                            size_t exp_bytes, hipStream_t stream);
 
-// Largest grid of the page-balanced schedule: it bounds the chunks per KV
-// head, hence the partial slots the host reserves.
-constexpr int32_t kBalancedGridCap = 1024;
-// Pages per chunk of the page-balanced schedule (the device clamps to these).
+// Largest grid of the page-balanced schedule (two workgroups per CU on the
+// 256 CUs of an MI355X) and its waves per workgroup: they bound the page
+// ranges per KV head (one per wave), hence the partial slots the host
+// reserves.
+constexpr int32_t kBalancedGridCap = 512;
+constexpr int32_t kBalancedWaves = 4;
+// Pages per range of the page-balanced schedule (the device clamps to these).
 constexpr int32_t kMaxChunkPages = kMaxSplitPages;
 
 struct AttnLaunch {

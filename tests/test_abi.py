@@ -60,13 +60,14 @@ def test_split_and_workspace_queries():
     tickets = (pairs * 4 + 255) // 256 * 256
     ml = (pairs * S * g * 8 + 255) // 256 * 256
     assert ws == tickets + ml + pairs * S * g * 128 * 4
-    # the 4-wave shape with the automatic split: page-balanced chunks, whose
-    # partial slots per KV head are bounded by the grid's share of chunks
-    # (1024 / Hkv) or by the chunks of the largest size, plus one per sequence
+    # the 4-wave shape with the automatic split: page-balanced ranges, one per
+    # wave, whose partial slots per KV head are bounded by the grid's share of
+    # ranges (512 / Hkv workgroups x 4 waves) or by the ranges of the largest
+    # size, plus one per sequence
     B, Hkv, g, ctx = 64, 8, 5, 15192
     assert hma.tokens_per_split(B, Hkv * g, Hkv, ctx) == 2048
     pages = -(-ctx // 16)
-    slots = Hkv * (max(1024 // Hkv, -(-B * pages // 1024)) + B)
+    slots = Hkv * (max(512 // Hkv * 4, -(-B * pages // 1024)) + B)
     assert hma.workspace_bytes(B, Hkv * g, Hkv, ctx) == (
         (B * Hkv * 4 + 255) // 256 * 256 + (slots * g * 8 + 255) // 256 * 256 + slots * g * 128 * 4)
     # the same shape with an explicit split: one slot per (sequence, head, split)

@@ -197,6 +197,29 @@ def test_full_size_workload_sampled(index, n_seq):
     note(f"attn: {w.name} max abs err {err:.3g} on {len(seqs)} sequences")
 
 
+def test_trace_mix_pure_bfp8_one_range_per_wave():
+    """The 200-sequence trace mix with BFP8 pages only: the pure-BFP8 kernel
+    under the page-balanced schedule at its one-range-per-wave granularity
+    (taken for ranges of at least 128 pages; here T / (64 workgroups per KV
+    head x 4 waves) pages each), where every piece is attended and published
+    by one wave and the last wave to arrive folds.  Sampled sequences against
+    the oracle, and a repeat call bitwise equal (the fold runs in piece order
+    whichever wave arrives last)."""
+    w = wl.WORKLOADS[4]
+    seqs = _sample_seqs(w, 8, seed=40)
+    kv = make_paged(w, bf16_fraction=0.0, with_bf16_pool=False, value_seqs=seqs)
+    T = int(wl.pages_per_seq(kv.ctx, w.page_size).sum())
+    assert -(-T // (512 // w.num_kv_heads * 4)) >= 128
+    note(f"attn: trace mix, BFP8 only, {T} pages per KV head")
+    d = DevKV(kv)
+    out, lse = d.attn()
+    out2, lse2 = d.attn()
+    assert torch.equal(out, out2) and torch.equal(lse, lse2)
+    ref, ref_lse = _oracle_rows(kv, seqs)
+    err = assert_attn_close(out, lse, ref, ref_lse, rows=seqs, what="trace mix BFP8")
+    note(f"attn: trace mix BFP8 max abs err {err:.3g} on {len(seqs)} sequences")
+
+
 def test_single_long_sequence_many_splits():
     """One 32K-token sequence (Qwen3-32B heads): the automatic split gives 32
     splits of 1024 tokens on 256 one-per-CU workgroups, so the last workgroup
