@@ -10,7 +10,7 @@ import torch
 import oracle
 import paper_2606_29986_amd as hma
 
-# spec tolerance for the BF16 attention output against the float64 oracle
+# tolerance for the BF16 attention output against the float64 oracle (absolute + relative)
 ATOL = 2e-3
 RTOL = 1e-2
 # LSE (float32): scores are exact products summed in float32 and the softmax
