@@ -387,6 +387,25 @@ def read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident,
     return out
 
 
+def issue_ceiling(hma, torch, waves_per_simd=2, iters=2000):
+    """libhma's issue probe: shader-clock cycles of one step (eight times one
+    16x16x32 BF16 matrix instruction and/or VALU adds) with waves_per_simd
+    waves on every SIMD, median over the waves.  The fused attention issues
+    about 16 VALU instructions per matrix instruction."""
+    dev = torch.device("cuda", 0)
+    n = 1024 * waves_per_simd
+    cyc = torch.zeros(n, dtype=torch.int64, device=dev)
+    sink = torch.zeros(n * 64, dtype=torch.int32, device=dev)
+    out = {"waves_per_simd": waves_per_simd, "unit": "shader cycles per (matrix instruction + VALU group)"}
+    for valu, mfma in ((0, 1), (8, 0), (8, 1), (16, 0), (16, 1)):
+        hma.issue_probe(valu, mfma, waves_per_simd, 200, cyc, sink)     # warm-up
+        hma.issue_probe(valu, mfma, waves_per_simd, iters, cyc, sink)
+        torch.cuda.synchronize()
+        key = ("mfma" if mfma else "") + ("_plus_" if mfma and valu else "") + (f"valu{valu}" if valu else "")
+        out[key] = round(float(np.median(cyc.cpu().numpy())) / (iters * 8), 2)
+    return out
+
+
 def route_legs(w, hma, torch, total_pages, pt_d, ctx_d, max_ctx, q, tps, scale, stream, a_bytes):
     """One attention layer timed on codes that force the ldexp decode route
     (every page carries one block exponent of 134), against the headline's
@@ -809,6 +828,7 @@ def main():
     if legs:
         res["read_ceiling"] = read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident,
                                            stream, attn_mean)
+        res["issue_ceiling"] = issue_ceiling(hma, torch)
         res["route_legs"] = route_legs(w, hma, torch, total_pages, pt_d, ctx_d, max_ctx, q, tps_arg, scale,
                                        stream, a_bytes)
         if w.num_q_heads // w.num_kv_heads <= 8:

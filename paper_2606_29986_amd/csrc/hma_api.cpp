@@ -621,6 +621,25 @@ int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workgroups, u
                : HMA_EHIP;
 }
 
+int hma_issue_probe(int32_t valu_ops, int32_t with_mfma, int32_t waves_per_simd, int32_t iters, uint64_t *cycles,
+                    size_t cycles_words, uint32_t *sink, size_t sink_words, void *stream)
+{
+    if (!(valu_ops == 0 || valu_ops == 4 || valu_ops == 8 || valu_ops == 16) || (with_mfma != 0 && with_mfma != 1))
+        return HMA_EINVAL;
+    if (valu_ops == 0 && with_mfma == 0)
+        return HMA_EINVAL;
+    if (waves_per_simd < 1 || waves_per_simd > 4 || iters < 1 || iters > (1 << 20))
+        return HMA_EINVAL;
+    const int64_t n_waves = 4 * kComputeUnits * waves_per_simd;
+    if (!cycles || !sink || !aligned(cycles, 8) || !aligned(sink, 4) || cycles_words < (size_t)n_waves ||
+        sink_words < (size_t)n_waves * 64)
+        return HMA_EINVAL;
+    return hma::launch_issue_probe(valu_ops, with_mfma != 0, (int32_t)n_waves, iters, cycles, sink,
+                                   static_cast<hipStream_t>(stream)) == 0
+               ? HMA_OK
+               : HMA_EHIP;
+}
+
 size_t hma_decode_attn_valu_workspace_bytes(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads,
                                             int32_t max_context_len, int32_t tokens_per_split)
 {

@@ -1,5 +1,6 @@
-// read_probe.hip -- read-only probes: the HBM read ceiling that the fused
-// attention's page loop is measured against.
+// read_probe.hip -- measurement probes: the HBM read ceiling that the fused
+// attention's page loop is measured against, and the SIMD issue rate of
+// matrix and vector instructions mixed as in its loop.
 //
 // The paged probe reads exactly the bytes a decode-attention launch must read
 // (the BFP8 mantissa and exponent tiles of every page of every sequence, per
@@ -151,7 +152,89 @@ __global__ __launch_bounds__(kStreamThreads) void stream_read_probe_kernel(const
         sink[(uint64_t)blockIdx.x * (kStreamThreads / 64) + (threadIdx.x >> 6)] = x;
 }
 
+// Issue probe: one wave per workgroup, waves_per_simd of them on every SIMD;
+// each step of a wave issues, eight times over, one 16x16x32 BF16 matrix
+// instruction (eight independent accumulators) and/or VALU integer adds
+// (eight independent chains), written as inline assembly so that the compiler
+// neither drops nor reorders them.  A wave reports the shader-clock cycles
+// (s_memtime) of its whole loop; cycles / (iters * 8) is the time of one
+// (matrix instruction + VALU group) step on a SIMD shared with the other
+// waves.
+template <int VALU, bool MFMA>
+__global__ __launch_bounds__(64) void issue_probe_kernel(uint64_t *cycles, uint32_t *sink, int32_t iters)
+{
+    const uint32_t lane = threadIdx.x;
+    f32x4_t c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0, c4 = c0, c5 = c0, c6 = c0, c7 = c0;
+    const u32x4_t a = {lane, lane * 3u, 7u, 9u};
+    uint32_t x[8];
+#pragma unroll
+    for (int k = 0; k < 8; k++)
+        x[k] = lane * (2u * k + 1u);
+#define HMA_PROBE_MFMA(c)                                                                                       \
+    do {                                                                                                        \
+        if (MFMA)                                                                                               \
+            asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(c) : "v"(a), "v"(a));                \
+    } while (0)
+#define HMA_PROBE_VALU()                                                                                        \
+    do {                                                                                                        \
+        _Pragma("unroll") for (int k_ = 0; k_ < VALU; k_++)                                                     \
+            asm volatile("v_add_u32 %0, %0, %1" : "+v"(x[k_ & 7]) : "v"(lane));                                \
+    } while (0)
+    const uint64_t t0 = __builtin_amdgcn_s_memtime();
+    for (int it = 0; it < iters; it++) {
+        HMA_PROBE_MFMA(c0);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c1);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c2);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c3);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c4);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c5);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c6);
+        HMA_PROBE_VALU();
+        HMA_PROBE_MFMA(c7);
+        HMA_PROBE_VALU();
+    }
+    const uint64_t t1 = __builtin_amdgcn_s_memtime();
+#undef HMA_PROBE_MFMA
+#undef HMA_PROBE_VALU
+    const f32x4_t c = c0 + c1 + c2 + c3 + c4 + c5 + c6 + c7;
+    uint32_t xs = 0;
+#pragma unroll
+    for (int k = 0; k < 8; k++)
+        xs ^= x[k];
+    sink[(uint64_t)blockIdx.x * 64 + lane] = __float_as_uint(c.x + c.y + c.z + c.w) ^ xs;
+    if (lane == 0)
+        cycles[blockIdx.x] = t1 - t0;
+}
+
 }  // namespace
+
+int launch_issue_probe(int32_t valu_ops, bool mfma, int32_t n_waves, int32_t iters, uint64_t *cycles, uint32_t *sink,
+                       hipStream_t stream)
+{
+    const dim3 grid((uint32_t)n_waves), block(64);
+#define HMA_PROBE_LAUNCH(V)                                                                                     \
+    do {                                                                                                        \
+        if (mfma)                                                                                               \
+            hipLaunchKernelGGL((issue_probe_kernel<V, true>), grid, block, 0, stream, cycles, sink, iters);     \
+        else                                                                                                    \
+            hipLaunchKernelGGL((issue_probe_kernel<V, false>), grid, block, 0, stream, cycles, sink, iters);    \
+    } while (0)
+    switch (valu_ops) {
+    case 0: HMA_PROBE_LAUNCH(0); break;
+    case 4: HMA_PROBE_LAUNCH(4); break;
+    case 8: HMA_PROBE_LAUNCH(8); break;
+    case 16: HMA_PROBE_LAUNCH(16); break;
+    default: return -1;
+    }
+#undef HMA_PROBE_LAUNCH
+    return hipGetLastError() == hipSuccess ? 0 : -1;
+}
 
 int launch_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, const uint8_t *v_mant,
                             const uint8_t *v_exp, const int32_t *page_table, int32_t max_pages,

@@ -31,7 +31,8 @@ def test_header_declares_the_boundary():
                             "hma_decode_attn_tokens_per_split", "hma_decode_attn_workspace_bytes",
                             "hma_ingress_rebuild", "hma_status_string", "hma_validate_page_table",
                             "hma_paged_read_probe", "hma_stream_read_probe",
-                            "hma_decode_attn_bfp8_valu", "hma_decode_attn_valu_workspace_bytes"])
+                            "hma_decode_attn_bfp8_valu", "hma_decode_attn_valu_workspace_bytes",
+                            "hma_issue_probe"])
 
 
 def test_library_exports_every_declared_symbol():
@@ -386,3 +387,23 @@ def test_valu_attn_validation_and_workspace():
     assert call(q=MISALIGNED) == hma.HMA_EINVAL
     assert call(lse=0x10002) == hma.HMA_EINVAL
     assert call(Bn=0) == hma.HMA_OK
+
+
+def test_issue_probe_validation():
+    """hma_issue_probe rejects unsupported mixes and short buffers before any HIP call."""
+    L = hma.lib()
+
+    def call(valu=8, mfma=1, wps=2, iters=100, cyc=FAKE, cw=None, sink=FAKE, sw=None):
+        n = 1024 * wps
+        return L.hma_issue_probe(valu, mfma, wps, iters, cyc, n if cw is None else cw, sink,
+                                 n * 64 if sw is None else sw, None)
+    assert call(valu=3) == hma.HMA_EINVAL
+    assert call(valu=0, mfma=0) == hma.HMA_EINVAL
+    assert call(mfma=2) == hma.HMA_EINVAL
+    assert call(wps=0) == hma.HMA_EINVAL
+    assert call(wps=5) == hma.HMA_EINVAL
+    assert call(iters=0) == hma.HMA_EINVAL
+    assert call(cyc=None) == hma.HMA_EINVAL
+    assert call(cyc=FAKE + 4) == hma.HMA_EINVAL           # 8-byte words
+    assert call(cw=2047) == hma.HMA_EINVAL
+    assert call(sw=2048 * 64 - 1) == hma.HMA_EINVAL

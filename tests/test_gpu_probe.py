@@ -63,3 +63,24 @@ def test_stream_read_probe_reads_each_byte_once(nbytes, nwg):
     hma.stream_read_probe(torch.from_numpy(host).cuda(), sink, nwg)
     torch.cuda.synchronize()
     assert _xor_words(sink.cpu().numpy()) == _xor_words(host)
+
+
+def test_issue_probe_counts_cycles_on_every_wave():
+    """The issue probe: every wave reports a positive cycle count; one step of
+    a matrix instruction plus 8 adds takes at least as long as either alone
+    and no longer than both in sequence (plus a margin for the loop)."""
+    wps, iters = 2, 400
+    n = 1024 * wps
+    cyc = torch.zeros(n, dtype=torch.int64, device="cuda")
+    sink = torch.zeros(n * 64, dtype=torch.int32, device="cuda")
+    per = {}
+    for valu, mfma in ((0, 1), (8, 0), (8, 1)):
+        note(f"issue probe valu={valu} mfma={mfma}")
+        cyc.zero_()
+        hma.issue_probe(valu, mfma, wps, iters, cyc, sink)
+        torch.cuda.synchronize()
+        c = cyc.cpu().numpy()
+        assert (c > 0).all(), (valu, mfma)
+        per[(valu, mfma)] = float(np.median(c)) / (iters * 8)
+    assert per[(8, 1)] >= 0.9 * max(per[(0, 1)], per[(8, 0)])
+    assert per[(8, 1)] <= 1.1 * (per[(0, 1)] + per[(8, 0)]) + 4
