@@ -388,21 +388,27 @@ def read_ceiling(w, hma, torch, mant, expo, pt_d, ctx_d, max_ctx, tps, resident,
 
 
 def issue_ceiling(hma, torch, waves_per_simd=2, iters=2000):
-    """libhma's issue probe: shader-clock cycles of one step (eight times one
-    16x16x32 BF16 matrix instruction and/or VALU adds) with waves_per_simd
-    waves on every SIMD, median over the waves.  The fused attention issues
-    about 16 VALU instructions per matrix instruction."""
+    """libhma's issue probe with waves_per_simd waves on every SIMD.  A SIMD's
+    time is its last wave's (the older wave is favoured and finishes first),
+    so each figure is the largest per-wave cycle count over all the work the
+    SIMD's waves issued: SIMD cycles per step of one 16x16x32 BF16 matrix
+    instruction, of 8 plain adds, and of both; and SIMD cycles per
+    instruction of each VALU kind the decode and softmax issue."""
     dev = torch.device("cuda", 0)
     n = 1024 * waves_per_simd
     cyc = torch.zeros(n, dtype=torch.int64, device=dev)
     sink = torch.zeros(n * 64, dtype=torch.int32, device=dev)
-    out = {"waves_per_simd": waves_per_simd, "unit": "shader cycles per (matrix instruction + VALU group)"}
-    for valu, mfma in ((0, 1), (8, 0), (8, 1), (16, 0), (16, 1)):
-        hma.issue_probe(valu, mfma, waves_per_simd, 200, cyc, sink)     # warm-up
-        hma.issue_probe(valu, mfma, waves_per_simd, iters, cyc, sink)
+
+    def run(kind, valu, mfma):
+        hma.issue_probe(kind, valu, mfma, waves_per_simd, 200, cyc, sink)     # warm-up
+        hma.issue_probe(kind, valu, mfma, waves_per_simd, iters, cyc, sink)
         torch.cuda.synchronize()
-        key = ("mfma" if mfma else "") + ("_plus_" if mfma and valu else "") + (f"valu{valu}" if valu else "")
-        out[key] = round(float(np.median(cyc.cpu().numpy())) / (iters * 8), 2)
+        return float(cyc.max().item()) / (iters * 8) / waves_per_simd
+    out = {"waves_per_simd": waves_per_simd, "unit": "SIMD shader cycles (last wave)"}
+    out["mfma"] = round(run(0, 0, 1), 2)
+    out["valu8"] = round(run(0, 8, 0), 2)
+    out["mfma_plus_valu8"] = round(run(0, 8, 1), 2)
+    out["per_instruction"] = {name: round(run(k, 16, 0) / 16, 2) for k, name in enumerate(hma.ISSUE_KINDS)}
     return out
 
 

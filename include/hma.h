@@ -430,22 +430,26 @@ HMA_API int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workg
 
 /*
  * hma_issue_probe -- measurement, not part of the method: the SIMD issue rate
- * of matrix and vector instructions mixed as in the fused attention's loop.
- * Launches 4 x 256 x waves_per_simd one-wave workgroups (waves_per_simd
- * waves on each SIMD of the 256 CUs); each wave runs `iters` steps, each step
- * issuing eight times one v_mfma_f32_16x16x32_bf16 (with_mfma = 1, eight
- * independent accumulators) and valu_ops 32-bit integer adds (eight
- * independent chains), and writes the shader-clock cycles (s_memtime) of its
- * loop to cycles[wave]; cycles / (iters * 8) is one step's time on a SIMD
- * shared with the other waves.
- *   valu_ops        0, 4, 8 or 16; with_mfma 0 or 1, not both zero
+ * of matrix and vector instructions of the kinds the fused attention's loop
+ * issues.  Launches 4 x 256 x waves_per_simd one-wave workgroups
+ * (waves_per_simd waves on each SIMD of the 256 CUs); each wave runs `iters`
+ * steps, each step issuing eight times one v_mfma_f32_16x16x32_bf16
+ * (with_mfma = 1, eight independent accumulators) and valu_ops VALU
+ * instructions of one kind (eight independent chains), and writes the
+ * shader-clock cycles (s_memtime) of its loop to cycles[wave];
+ * cycles / (iters * 8) is one step's time on a SIMD shared with the other
+ * waves.
+ *   valu_kind       0 v_add_u32, 1 v_perm_b32, 2 v_cvt_f32_ubyte1,
+ *                   3 v_pk_sub_u16 (clamped), 4 v_fma_f32
+ *   valu_ops        0, 8 or 16; with_mfma 0 or 1, not both zero
  *   waves_per_simd  1..4; iters 1..1048576
  *   cycles          device uint64 [1024 * waves_per_simd]; cycles_words its length
  *   sink            device uint32 [1024 * waves_per_simd * 64] (results kept live)
  * Errors: HMA_EINVAL, HMA_EHIP.
  */
-HMA_API int hma_issue_probe(int32_t valu_ops, int32_t with_mfma, int32_t waves_per_simd, int32_t iters,
-                            uint64_t *cycles, size_t cycles_words, uint32_t *sink, size_t sink_words, void *stream);
+HMA_API int hma_issue_probe(int32_t valu_kind, int32_t valu_ops, int32_t with_mfma, int32_t waves_per_simd,
+                            int32_t iters, uint64_t *cycles, size_t cycles_words, uint32_t *sink, size_t sink_words,
+                            void *stream);
 
 /*
  * hma_decode_attn_bfp8_valu -- measurement, not for production: the fused

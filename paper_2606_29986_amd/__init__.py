@@ -79,7 +79,7 @@ def lib() -> ctypes.CDLL:
     L.hma_decode_attn_bfp8_valu.restype = ctypes.c_int
     L.hma_decode_attn_valu_workspace_bytes.argtypes = [i32, i32, i32, i32, i32]
     L.hma_decode_attn_valu_workspace_bytes.restype = sz
-    L.hma_issue_probe.argtypes = [i32, i32, i32, i32, vp, sz, vp, sz, vp]
+    L.hma_issue_probe.argtypes = [i32, i32, i32, i32, i32, vp, sz, vp, sz, vp]
     L.hma_issue_probe.restype = ctypes.c_int
     L.hma_status_string.argtypes = [ctypes.c_int]
     L.hma_status_string.restype = ctypes.c_char_p
@@ -305,14 +305,17 @@ def decode_attn_bfp8_noalloc(q, k_mant, k_exp, v_mant, v_exp, page_table, contex
         raise HmaError(rc, "hma_decode_attn_bfp8_noalloc")
 
 
-def issue_probe(valu_ops, with_mfma, waves_per_simd, iters, cycles, sink, stream=None) -> None:
+ISSUE_KINDS = ("v_add_u32", "v_perm_b32", "v_cvt_f32_ubyte1", "v_pk_sub_u16", "v_fma_f32")
+
+
+def issue_probe(valu_kind, valu_ops, with_mfma, waves_per_simd, iters, cycles, sink, stream=None) -> None:
     """hma_issue_probe: cycles (int64/uint64 device tensor, 1024 * waves_per_simd
     words) receives each wave's shader-clock cycles over `iters` steps of
-    eight (matrix instruction + valu_ops adds) groups; sink holds 64 words per
-    wave."""
+    eight (matrix instruction + valu_ops instructions of ISSUE_KINDS[valu_kind])
+    groups; sink holds 64 words per wave."""
     _check_dev(cycles, sink)
-    rc = lib().hma_issue_probe(int(valu_ops), int(with_mfma), int(waves_per_simd), int(iters), _ptr(cycles),
-                               int(cycles.numel()), _ptr(sink), int(sink.numel()), _stream(stream))
+    rc = lib().hma_issue_probe(int(valu_kind), int(valu_ops), int(with_mfma), int(waves_per_simd), int(iters),
+                               _ptr(cycles), int(cycles.numel()), _ptr(sink), int(sink.numel()), _stream(stream))
     if rc != HMA_OK:
         raise HmaError(rc, "hma_issue_probe")
 

@@ -621,10 +621,11 @@ int hma_stream_read_probe(const void *buf, size_t bytes, int32_t n_workgroups, u
                : HMA_EHIP;
 }
 
-int hma_issue_probe(int32_t valu_ops, int32_t with_mfma, int32_t waves_per_simd, int32_t iters, uint64_t *cycles,
-                    size_t cycles_words, uint32_t *sink, size_t sink_words, void *stream)
+int hma_issue_probe(int32_t valu_kind, int32_t valu_ops, int32_t with_mfma, int32_t waves_per_simd, int32_t iters,
+                    uint64_t *cycles, size_t cycles_words, uint32_t *sink, size_t sink_words, void *stream)
 {
-    if (!(valu_ops == 0 || valu_ops == 4 || valu_ops == 8 || valu_ops == 16) || (with_mfma != 0 && with_mfma != 1))
+    if (valu_kind < 0 || valu_kind > 4 || !(valu_ops == 0 || valu_ops == 8 || valu_ops == 16) ||
+        (with_mfma != 0 && with_mfma != 1))
         return HMA_EINVAL;
     if (valu_ops == 0 && with_mfma == 0)
         return HMA_EINVAL;
@@ -634,7 +635,7 @@ int hma_issue_probe(int32_t valu_ops, int32_t with_mfma, int32_t waves_per_simd,
     if (!cycles || !sink || !aligned(cycles, 8) || !aligned(sink, 4) || cycles_words < (size_t)n_waves ||
         sink_words < (size_t)n_waves * 64)
         return HMA_EINVAL;
-    return hma::launch_issue_probe(valu_ops, with_mfma != 0, (int32_t)n_waves, iters, cycles, sink,
+    return hma::launch_issue_probe(valu_kind, valu_ops, with_mfma != 0, (int32_t)n_waves, iters, cycles, sink,
                                    static_cast<hipStream_t>(stream)) == 0
                ? HMA_OK
                : HMA_EHIP;

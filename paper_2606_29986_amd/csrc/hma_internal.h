@@ -97,10 +97,10 @@ int launch_paged_read_probe(const uint8_t *k_mant, const uint8_t *k_exp, const u
                             hipStream_t stream);
 int launch_stream_read_probe(const void *buf, uint64_t bytes, uint32_t *sink, int32_t n_workgroups,
                              hipStream_t stream);
-// Issue probe (read_probe.hip): n_waves one-wave workgroups; valu_ops in
-// {0, 4, 8, 16}; cycles[w] and sink[w * 64 + lane] written per wave.
-int launch_issue_probe(int32_t valu_ops, bool mfma, int32_t n_waves, int32_t iters, uint64_t *cycles, uint32_t *sink,
-                       hipStream_t stream);
+// Issue probe (read_probe.hip): n_waves one-wave workgroups; kind 0..4,
+// valu_ops in {0, 8, 16}; cycles[w] and sink[w * 64 + lane] written per wave.
+int launch_issue_probe(int32_t kind, int32_t valu_ops, bool mfma, int32_t n_waves, int32_t iters, uint64_t *cycles,
+                       uint32_t *sink, hipStream_t stream);
 
 // Vector-ALU decode attention (valu_attn.hip): per split a partial kernel
 // (grid batch * hkv * n_splits), then a merge kernel (grid batch * hkv).

@@ -154,22 +154,28 @@ __global__ __launch_bounds__(kStreamThreads) void stream_read_probe_kernel(const
 
 // Issue probe: one wave per workgroup, waves_per_simd of them on every SIMD;
 // each step of a wave issues, eight times over, one 16x16x32 BF16 matrix
-// instruction (eight independent accumulators) and/or VALU integer adds
-// (eight independent chains), written as inline assembly so that the compiler
-// neither drops nor reorders them.  A wave reports the shader-clock cycles
-// (s_memtime) of its whole loop; cycles / (iters * 8) is the time of one
-// (matrix instruction + VALU group) step on a SIMD shared with the other
-// waves.
-template <int VALU, bool MFMA>
+// instruction (eight independent accumulators) and/or VALU instructions of
+// one kind (eight independent chains), written as inline assembly so that
+// the compiler neither drops nor reorders them.  Kinds: 0 v_add_u32,
+// 1 v_perm_b32, 2 v_cvt_f32_ubyte1, 3 v_pk_sub_u16 (clamped), 4 v_fma_f32
+// (the first and last are plain ALU operations, the middle three are the
+// block-float decode's).  A wave reports the shader-clock cycles (s_memtime)
+// of its whole loop; cycles / (iters * 8) is the time of one step on a SIMD
+// shared with the other waves.
+template <int KIND, int VALU, bool MFMA>
 __global__ __launch_bounds__(64) void issue_probe_kernel(uint64_t *cycles, uint32_t *sink, int32_t iters)
 {
     const uint32_t lane = threadIdx.x;
     f32x4_t c0 = {0.f, 0.f, 0.f, 0.f}, c1 = c0, c2 = c0, c3 = c0, c4 = c0, c5 = c0, c6 = c0, c7 = c0;
     const u32x4_t a = {lane, lane * 3u, 7u, 9u};
+    const uint32_t k1 = lane ^ 0x5A5A5A5Au, k2 = lane * 7u + 3u;
     uint32_t x[8];
+    float f[8];
 #pragma unroll
-    for (int k = 0; k < 8; k++)
+    for (int k = 0; k < 8; k++) {
         x[k] = lane * (2u * k + 1u);
+        f[k] = (float)(lane + k);
+    }
 #define HMA_PROBE_MFMA(c)                                                                                       \
     do {                                                                                                        \
         if (MFMA)                                                                                               \
@@ -177,8 +183,18 @@ __global__ __launch_bounds__(64) void issue_probe_kernel(uint64_t *cycles, uint3
     } while (0)
 #define HMA_PROBE_VALU()                                                                                        \
     do {                                                                                                        \
-        _Pragma("unroll") for (int k_ = 0; k_ < VALU; k_++)                                                     \
-            asm volatile("v_add_u32 %0, %0, %1" : "+v"(x[k_ & 7]) : "v"(lane));                                \
+        _Pragma("unroll") for (int k_ = 0; k_ < VALU; k_++) {                                                   \
+            if (KIND == 0)                                                                                      \
+                asm volatile("v_add_u32 %0, %0, %1" : "+v"(x[k_ & 7]) : "v"(k1));                              \
+            if (KIND == 1)                                                                                      \
+                asm volatile("v_perm_b32 %0, %0, %1, %2" : "+v"(x[k_ & 7]) : "v"(k1), "v"(k2));                \
+            if (KIND == 2)                                                                                      \
+                asm volatile("v_cvt_f32_ubyte1 %0, %1" : "=v"(f[k_ & 7]) : "v"(x[k_ & 7]));                    \
+            if (KIND == 3)                                                                                      \
+                asm volatile("v_pk_sub_u16 %0, %0, %1 clamp" : "+v"(x[k_ & 7]) : "v"(k1));                     \
+            if (KIND == 4)                                                                                      \
+                asm volatile("v_fma_f32 %0, %0, %1, %0" : "+v"(f[k_ & 7]) : "v"(k1));                          \
+        }                                                                                                       \
     } while (0)
     const uint64_t t0 = __builtin_amdgcn_s_memtime();
     for (int it = 0; it < iters; it++) {
@@ -206,7 +222,7 @@ __global__ __launch_bounds__(64) void issue_probe_kernel(uint64_t *cycles, uint3
     uint32_t xs = 0;
 #pragma unroll
     for (int k = 0; k < 8; k++)
-        xs ^= x[k];
+        xs ^= x[k] ^ __float_as_uint(f[k]);
     sink[(uint64_t)blockIdx.x * 64 + lane] = __float_as_uint(c.x + c.y + c.z + c.w) ^ xs;
     if (lane == 0)
         cycles[blockIdx.x] = t1 - t0;
@@ -214,25 +230,40 @@ __global__ __launch_bounds__(64) void issue_probe_kernel(uint64_t *cycles, uint3
 
 }  // namespace
 
-int launch_issue_probe(int32_t valu_ops, bool mfma, int32_t n_waves, int32_t iters, uint64_t *cycles, uint32_t *sink,
-                       hipStream_t stream)
+template <int KIND>
+static void launch_issue_kind(int32_t valu_ops, bool mfma, dim3 grid, dim3 block, int32_t iters, uint64_t *cycles,
+                              uint32_t *sink, hipStream_t stream)
 {
-    const dim3 grid((uint32_t)n_waves), block(64);
 #define HMA_PROBE_LAUNCH(V)                                                                                     \
     do {                                                                                                        \
         if (mfma)                                                                                               \
-            hipLaunchKernelGGL((issue_probe_kernel<V, true>), grid, block, 0, stream, cycles, sink, iters);     \
+            hipLaunchKernelGGL((issue_probe_kernel<KIND, V, true>), grid, block, 0, stream, cycles, sink, iters); \
         else                                                                                                    \
-            hipLaunchKernelGGL((issue_probe_kernel<V, false>), grid, block, 0, stream, cycles, sink, iters);    \
+            hipLaunchKernelGGL((issue_probe_kernel<KIND, V, false>), grid, block, 0, stream, cycles, sink, iters); \
     } while (0)
-    switch (valu_ops) {
-    case 0: HMA_PROBE_LAUNCH(0); break;
-    case 4: HMA_PROBE_LAUNCH(4); break;
-    case 8: HMA_PROBE_LAUNCH(8); break;
-    case 16: HMA_PROBE_LAUNCH(16); break;
+    if (valu_ops == 0)
+        HMA_PROBE_LAUNCH(0);
+    else if (valu_ops == 8)
+        HMA_PROBE_LAUNCH(8);
+    else
+        HMA_PROBE_LAUNCH(16);
+#undef HMA_PROBE_LAUNCH
+}
+
+int launch_issue_probe(int32_t kind, int32_t valu_ops, bool mfma, int32_t n_waves, int32_t iters, uint64_t *cycles,
+                       uint32_t *sink, hipStream_t stream)
+{
+    const dim3 grid((uint32_t)n_waves), block(64);
+    if (valu_ops != 0 && valu_ops != 8 && valu_ops != 16)
+        return -1;
+    switch (kind) {
+    case 0: launch_issue_kind<0>(valu_ops, mfma, grid, block, iters, cycles, sink, stream); break;
+    case 1: launch_issue_kind<1>(valu_ops, mfma, grid, block, iters, cycles, sink, stream); break;
+    case 2: launch_issue_kind<2>(valu_ops, mfma, grid, block, iters, cycles, sink, stream); break;
+    case 3: launch_issue_kind<3>(valu_ops, mfma, grid, block, iters, cycles, sink, stream); break;
+    case 4: launch_issue_kind<4>(valu_ops, mfma, grid, block, iters, cycles, sink, stream); break;
     default: return -1;
     }
-#undef HMA_PROBE_LAUNCH
     return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 

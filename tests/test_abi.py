@@ -393,11 +393,14 @@ def test_issue_probe_validation():
     """hma_issue_probe rejects unsupported mixes and short buffers before any HIP call."""
     L = hma.lib()
 
-    def call(valu=8, mfma=1, wps=2, iters=100, cyc=FAKE, cw=None, sink=FAKE, sw=None):
+    def call(kind=0, valu=8, mfma=1, wps=2, iters=100, cyc=FAKE, cw=None, sink=FAKE, sw=None):
         n = 1024 * wps
-        return L.hma_issue_probe(valu, mfma, wps, iters, cyc, n if cw is None else cw, sink,
+        return L.hma_issue_probe(kind, valu, mfma, wps, iters, cyc, n if cw is None else cw, sink,
                                  n * 64 if sw is None else sw, None)
     assert call(valu=3) == hma.HMA_EINVAL
+    assert call(valu=4) == hma.HMA_EINVAL
+    assert call(kind=-1) == hma.HMA_EINVAL
+    assert call(kind=5) == hma.HMA_EINVAL
     assert call(valu=0, mfma=0) == hma.HMA_EINVAL
     assert call(mfma=2) == hma.HMA_EINVAL
     assert call(wps=0) == hma.HMA_EINVAL

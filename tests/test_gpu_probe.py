@@ -66,21 +66,23 @@ def test_stream_read_probe_reads_each_byte_once(nbytes, nwg):
 
 
 def test_issue_probe_counts_cycles_on_every_wave():
-    """The issue probe: every wave reports a positive cycle count; one step of
-    a matrix instruction plus 8 adds takes at least as long as either alone
-    and no longer than both in sequence (plus a margin for the loop)."""
+    """The issue probe: every wave reports a positive cycle count, for every
+    instruction kind; one step of a matrix instruction plus 8 adds takes at
+    least as long as either alone and no longer than both in sequence (plus a
+    margin for the loop)."""
     wps, iters = 2, 400
     n = 1024 * wps
     cyc = torch.zeros(n, dtype=torch.int64, device="cuda")
     sink = torch.zeros(n * 64, dtype=torch.int32, device="cuda")
     per = {}
-    for valu, mfma in ((0, 1), (8, 0), (8, 1)):
-        note(f"issue probe valu={valu} mfma={mfma}")
+    cases = [(0, 0, 1), (0, 8, 0), (0, 8, 1)] + [(k, 16, 0) for k in range(1, len(hma.ISSUE_KINDS))]
+    for kind, valu, mfma in cases:
+        note(f"issue probe kind={kind} valu={valu} mfma={mfma}")
         cyc.zero_()
-        hma.issue_probe(valu, mfma, wps, iters, cyc, sink)
+        hma.issue_probe(kind, valu, mfma, wps, iters, cyc, sink)
         torch.cuda.synchronize()
         c = cyc.cpu().numpy()
-        assert (c > 0).all(), (valu, mfma)
-        per[(valu, mfma)] = float(np.median(c)) / (iters * 8)
-    assert per[(8, 1)] >= 0.9 * max(per[(0, 1)], per[(8, 0)])
-    assert per[(8, 1)] <= 1.1 * (per[(0, 1)] + per[(8, 0)]) + 4
+        assert (c > 0).all(), (kind, valu, mfma)
+        per[(kind, valu, mfma)] = float(np.median(c)) / (iters * 8)
+    assert per[(0, 8, 1)] >= 0.9 * max(per[(0, 0, 1)], per[(0, 8, 0)])
+    assert per[(0, 8, 1)] <= 1.1 * (per[(0, 0, 1)] + per[(0, 8, 0)]) + 4
