@@ -240,7 +240,7 @@ HMA_API int hma_ingress_rebuild(const uint8_t *host_mant, const uint8_t *host_ex
  *     whole batch, per KV head and in sequence order, into equal chunks
  *     built on the device from the lengths, for a grid of min(2, resident
  *     workgroups per CU) x CUs: one chunk per wave when that gives chunks of
- *     at least 128 pages (each wave then attends its pieces alone), else one
+ *     at least 64 pages (each wave then attends its pieces alone), else one
  *     per workgroup; a chunk that spans several sequences yields one range
  *     per sequence.  Ragged batches therefore load every compute unit
  *     equally.  Otherwise the ranges are tokens_per_split tokens of the

@@ -1134,7 +1134,7 @@ __device__ __forceinline__ Plan build_plan(const AttnParams &p, int32_t *sm_ctx,
 // timing.
 constexpr int kMinChunkPages = 16;
 constexpr int kMinWavePages = 4;
-constexpr int kWaveRangePages = 128;
+constexpr int kWaveRangePages = 64;
 
 __device__ __forceinline__ void balanced_schedule_table(const AttnParams &p, int32_t *sm_pre)
 {

@@ -200,7 +200,7 @@ def test_full_size_workload_sampled(index, n_seq):
 def test_trace_mix_pure_bfp8_one_range_per_wave():
     """The 200-sequence trace mix with BFP8 pages only: the pure-BFP8 kernel
     under the page-balanced schedule at its one-range-per-wave granularity
-    (taken for ranges of at least 128 pages; here T / (64 workgroups per KV
+    (taken for ranges of at least 64 pages; here T / (64 workgroups per KV
     head x 4 waves) pages each), where every piece is attended and published
     by one wave and the last wave to arrive folds.  Sampled sequences against
     the oracle, and a repeat call bitwise equal (the fold runs in piece order
@@ -209,7 +209,7 @@ def test_trace_mix_pure_bfp8_one_range_per_wave():
     seqs = _sample_seqs(w, 8, seed=40)
     kv = make_paged(w, bf16_fraction=0.0, with_bf16_pool=False, value_seqs=seqs)
     T = int(wl.pages_per_seq(kv.ctx, w.page_size).sum())
-    assert -(-T // (512 // w.num_kv_heads * 4)) >= 128
+    assert -(-T // (512 // w.num_kv_heads * 4)) >= 64
     note(f"attn: trace mix, BFP8 only, {T} pages per KV head")
     d = DevKV(kv)
     out, lse = d.attn()
